@@ -1,0 +1,145 @@
+"""Seeded synthetic inputs for the Gated DeltaNet prefill and decode paths.
+
+This module is shared by the tests, the benchmark and the smoke check, and it
+feeds both the HIP library and the CPU oracle. It holds only input
+distributions -- no step of the recurrence itself.
+
+Distributions (the paper publishes no workloads, so these stand in for the
+contest's 54 decode and 100 prefill workloads):
+
+* q, k ~ N(0, 1), L2-normalised per (token, head); q is further scaled by
+  1/sqrt(d_k) (the recurrence itself has no scale).
+* v ~ N(0, 1).
+* g = -softplus(N(mu, 1)) is the log of the per-token decay, alpha = exp(g);
+  mu = 0 gives a mean alpha of 0.50, mu = 1 (strong decay) 0.30, mu = -4 a weak
+  decay (alpha ~ 0.98) that keeps the state carry visible in the outputs.
+* beta = sigmoid(N(0, 1)).
+* initial states ~ N(0, 0.1^2) where present.
+* q, k, v are produced in fp32 and rounded to bf16 (round to nearest even)
+  when the workload is bf16; g, beta and states stay fp32.
+
+One numpy PCG64 stream per workload, seeded explicitly; draw order: sequence
+lengths, q, k, v, g noise, beta noise, initial state.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional, Tuple
+
+import numpy as np
+import torch
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    kind: str                       # "prefill" or "decode"
+    n_seqs: int                     # sequences (prefill) or batch (decode)
+    hqk: int
+    hv: int
+    d: int                          # d_k = d_v
+    chunk: int = 64
+    dtype: str = "bf16"             # element type of q, k, v, o
+    seq_len: Optional[int] = None   # fixed length per sequence
+    len_range: Optional[Tuple[int, int]] = None  # inclusive range, drawn
+    lengths: Optional[Tuple[int, ...]] = None    # explicit lengths
+    g_mu: float = 0.0
+    g_zero: bool = False            # alpha = 1 exactly
+    g_scale: float = 1.0            # multiplies g (stress: very strong decay)
+    state_std: float = 0.0          # 0 -> no initial state
+    seed: int = 1000
+
+    def replace(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+# The five workloads of the study, by what they are.
+PREFILL_TINY = Workload("prefill_tiny_T64_d32_f32", "prefill", n_seqs=1, hqk=1,
+                        hv=1, d=32, chunk=16, dtype="f32", seq_len=64,
+                        seed=1000)
+DECODE_B64 = Workload("decode_B64_hqk16_hv32_d128", "decode", n_seqs=64,
+                      hqk=16, hv=32, d=128, state_std=0.1, seed=1001)
+PREFILL_4K = Workload("prefill_T4096_hqk16_hv32_d128_C64", "prefill", n_seqs=1,
+                      hqk=16, hv=32, d=128, chunk=64, seq_len=4096, seed=1002)
+PREFILL_VARLEN = Workload("prefill_varlen16_U64-8192_hqk16_hv32_d128_C64",
+                          "prefill", n_seqs=16, hqk=16, hv=32, d=128, chunk=64,
+                          len_range=(64, 8192), state_std=0.1, seed=1003)
+PREFILL_LONG = Workload("prefill_2x32768_strongdecay_hqk16_hv32_d128_C64",
+                        "prefill", n_seqs=2, hqk=16, hv=32, d=128, chunk=64,
+                        seq_len=32768, g_mu=1.0, seed=1004)
+
+WORKLOADS = {w.name: w for w in
+             (PREFILL_TINY, DECODE_B64, PREFILL_4K, PREFILL_VARLEN,
+              PREFILL_LONG)}
+
+
+def _unit_rows(x: np.ndarray) -> np.ndarray:
+    n = np.sqrt(np.sum(x.astype(np.float64) ** 2, axis=-1, keepdims=True))
+    return (x / np.maximum(n, 1e-30)).astype(np.float32)
+
+
+def _softplus(x: np.ndarray) -> np.ndarray:
+    return np.logaddexp(0.0, x.astype(np.float64))
+
+
+def _sigmoid(x: np.ndarray) -> np.ndarray:
+    return 1.0 / (1.0 + np.exp(-x.astype(np.float64)))
+
+
+def _to_torch(x: np.ndarray, dtype: str) -> torch.Tensor:
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+
+def seq_lengths(w: Workload, rng: Optional[np.random.Generator] = None):
+    if w.lengths is not None:
+        return np.asarray(w.lengths, dtype=np.int64)
+    if w.seq_len is not None:
+        return np.full(w.n_seqs, w.seq_len, dtype=np.int64)
+    if w.len_range is not None:
+        assert rng is not None
+        lo, hi = w.len_range
+        return rng.integers(lo, hi + 1, size=w.n_seqs).astype(np.int64)
+    if w.kind == "decode":
+        return np.ones(w.n_seqs, dtype=np.int64)
+    raise ValueError("workload %s has no length rule" % w.name)
+
+
+def make(w: Workload, seed: Optional[int] = None) -> dict:
+    """Draw one input set for workload ``w`` as CPU torch tensors.
+
+    Returns a dict with q, k, v (bf16 or f32), g, beta (f32), cu_seqlens
+    (int32, prefill only), initial_state (f32 or None; for decode the state
+    that is advanced in place) and the workload itself under "w".
+    """
+    rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
+    lens = seq_lengths(w, rng)
+    T = int(lens.sum())
+    d = w.d
+    q = _unit_rows(rng.standard_normal((T, w.hqk, d), dtype=np.float32))
+    q = (q / np.float32(np.sqrt(d))).astype(np.float32)
+    k = _unit_rows(rng.standard_normal((T, w.hqk, d), dtype=np.float32))
+    v = rng.standard_normal((T, w.hv, d), dtype=np.float32)
+    gz = rng.standard_normal((T, w.hv), dtype=np.float32)
+    bz = rng.standard_normal((T, w.hv), dtype=np.float32)
+    if w.g_zero:
+        g = np.zeros((T, w.hv), dtype=np.float32)
+    else:
+        g = (-w.g_scale * _softplus(gz + np.float32(w.g_mu))).astype(np.float32)
+    beta = _sigmoid(bz).astype(np.float32)
+    n_states = w.n_seqs
+    s0 = None
+    if w.state_std > 0:
+        s0 = (w.state_std * rng.standard_normal((n_states, w.hv, d, d),
+                                                dtype=np.float32))
+        s0 = torch.from_numpy(s0.astype(np.float32))
+    cu = np.zeros(w.n_seqs + 1, dtype=np.int32)
+    cu[1:] = np.cumsum(lens)
+    out = dict(w=w, q=_to_torch(q, w.dtype), k=_to_torch(k, w.dtype),
+               v=_to_torch(v, w.dtype), g=torch.from_numpy(g),
+               beta=torch.from_numpy(beta), initial_state=s0,
+               cu_seqlens=torch.from_numpy(cu))
+    if w.kind == "decode":
+        if s0 is None:
+            out["initial_state"] = torch.zeros(w.n_seqs, w.hv, d, d)
+    return out
