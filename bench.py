@@ -1,0 +1,181 @@
+"""Benchmark: Gated DeltaNet prefill + decode on one MI355X.
+
+One step = one gdn_prefill over the 4096-token workload (1 sequence, 16 q/k
+heads, 32 v heads, d = 128, chunk 64, bf16) followed by one gdn_decode over the
+batch-64 workload (same heads, fp32 state updated in place). Inputs are
+resident in HBM before the timed region; three input sets are rotated so
+that consecutive steps never re-read data the 256 MB Infinity Cache could
+still hold. Each call is bracketed by HIP events on the stream it runs on.
+
+Prints one JSON line. `value` is prefill tokens/s (sum of the timed prefill
+calls); decode latency and HBM rate ride alongside. Roofline figures use
+fixed algorithmic counts:
+  prefill flop per token per value head = 6 d^2 + (6 + 4 HQK/HV) C d + C^2/3
+  prefill bytes = T (2 HQK d e + 2 HV d e + 8 HV) + N HV d^2 4 (1 + [S0])
+                  + 4 (N + 1)
+  decode bytes  = 2 B HV d^2 4 + B (2 HQK + 2 HV) d 2 + 8 B HV
+"""
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 matrix peak
+METRIC = "prefill tokens/sec + MFMA util; decode µs/step + achieved HBM GB/s"
+
+
+def prefill_flops(T, hqk, hv, d, C):
+    return float(T) * hv * (6 * d * d + (6 + 4.0 * hqk / hv) * C * d + C * C / 3.0)
+
+
+def prefill_bytes(T, N, hqk, hv, d, e, has_s0):
+    return (T * (2 * hqk * d * e + 2 * hv * d * e + 8 * hv)
+            + N * hv * d * d * 4 * (1 + int(has_s0)) + 4 * (N + 1))
+
+
+def decode_bytes(B, hqk, hv, d):
+    return 2 * B * hv * d * d * 4 + B * (2 * hqk + 2 * hv) * d * 2 + 8 * B * hv
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--rotate", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only (the recurrence has no "
+              "cross-GPU step here); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_16831_amd import gdn, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    wp, wd = synth.PREFILL_4K, synth.DECODE_B64
+
+    # ---------------------------------------------------------------- inputs
+    P, D = [], []
+    for r in range(args.rotate):
+        x = synth.make(wp, seed=wp.seed + 100 * r)
+        s = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in x.items()}
+        T = s["q"].shape[0]
+        s["o"] = torch.empty((T, wp.hv, wp.d), dtype=torch.bfloat16, device=dev)
+        s["fs"] = torch.empty((wp.n_seqs, wp.hv, wp.d, wp.d), device=dev)
+        s["ws"] = gdn.alloc_workspace(wp.n_seqs, T, wp.hqk, wp.hv, wp.d, wp.chunk, dev)
+        P.append(s)
+        y = synth.make(wd, seed=wd.seed + 100 * r)
+        t = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in y.items()}
+        t["o"] = torch.empty((wd.n_seqs, wd.hv, wd.d), dtype=torch.bfloat16, device=dev)
+        D.append(t)
+    torch.cuda.synchronize()
+
+    def run_prefill(s):
+        gdn.prefill(s["q"], s["k"], s["v"], s["g"], s["beta"], s["cu_seqlens"],
+                    initial_state=s["initial_state"], chunk=wp.chunk, o=s["o"],
+                    final_state=s["fs"], workspace=s["ws"])
+
+    def run_decode(t):
+        gdn.decode(t["q"], t["k"], t["v"], t["g"], t["beta"], t["initial_state"], o=t["o"])
+
+    for i in range(args.warmup):
+        run_prefill(P[i % args.rotate])
+        run_decode(D[i % args.rotate])
+    torch.cuda.synchronize()
+
+    # ---------------------------------------------------------------- timed
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(K):
+        e = ev[i]
+        e[0].record()
+        run_prefill(P[i % args.rotate])
+        e[1].record()
+        run_decode(D[i % args.rotate])
+        e[2].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+
+    pre_ms = [ev[i][0].elapsed_time(ev[i][1]) for i in range(K)]
+    dec_ms = [ev[i][1].elapsed_time(ev[i][2]) for i in range(K)]
+    pre_s = sum(pre_ms) / 1e3
+    dec_s = sum(dec_ms) / 1e3
+    T = P[0]["q"].shape[0]
+    pre_avg = pre_s / K
+    dec_avg = dec_s / K
+    pre_tps = K * T / pre_s
+    flop = prefill_flops(T, wp.hqk, wp.hv, wp.d, wp.chunk)
+    pbytes = prefill_bytes(T, wp.n_seqs, wp.hqk, wp.hv, wp.d, 2, False)
+    dbytes = decode_bytes(wd.n_seqs, wd.hqk, wd.hv, wd.d)
+    pre_tflops = flop / pre_avg / 1e12
+    dec_gbs = dbytes / dec_avg / 1e9
+
+    roof_pre = {"bound": "mfma", "achieved": round(pre_tflops, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "kernel": "gdn_prefill (chunk_offsets + chunk_local + chunk_carry)",
+                "algorithmic_flop_per_launch": flop,
+                "hbm_view_gbs": round(pbytes / pre_avg / 1e9, 1)}
+    roof_dec = {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(dec_gbs / PEAK_HBM_GBS, 4),
+                "traffic": None, "kernel": "decode_kernel<128, bf16>",
+                "algorithmic_bytes_per_launch": dbytes}
+    dominant = roof_dec if dec_avg >= pre_avg else roof_pre
+
+    pct = lambda xs, q: sorted(xs)[min(len(xs) - 1, int(q * len(xs)))]
+    out = {
+        "metric": METRIC, "value": round(pre_tps, 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / K, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "prefill %s + decode %s" % (wp.name, wd.name),
+                   "prefill_tokens": T, "decode_batch": wd.n_seqs,
+                   "heads_qk_v": [wp.hqk, wp.hv], "d": wp.d, "chunk": wp.chunk,
+                   "rotating_input_sets": args.rotate},
+        "prefill": {"us_per_call": round(pre_avg * 1e6, 2),
+                    "us_p10_p90": [round(pct(pre_ms, .1) * 1e3, 2), round(pct(pre_ms, .9) * 1e3, 2)],
+                    "tokens_per_s": round(pre_tps, 1), "tflops": round(pre_tflops, 2),
+                    "mfma_util": round(pre_tflops / PEAK_BF16_TFLOPS, 4)},
+        "decode": {"us_per_step": round(dec_avg * 1e6, 2),
+                   "us_p10_p90": [round(pct(dec_ms, .1) * 1e3, 2), round(pct(dec_ms, .9) * 1e3, 2)],
+                   "hbm_gbs": round(dec_gbs, 1), "hbm_frac": round(dec_gbs / PEAK_HBM_GBS, 4)},
+        "roofline": dominant,
+        "rooflines": [roof_pre, roof_dec],
+    }
+
+    # ---------------------------------------------------------------- oracle
+    if not args.no_cpu_baseline:
+        import oracle
+        x = synth.make(wp)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            oracle.prefill(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu_seqlens"],
+                           x["initial_state"])
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= args.cpu_seconds or reps >= 20:
+                break
+        out["cpu_baseline"] = {
+            "value": round(reps * T / el, 1), "unit": "tokens/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "%d full runs of the 4096-token prefill (all 32 heads), fp64 "
+                      "token-serial, %.1f s wall on %s" % (reps, el, platform.processor() or platform.machine())}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

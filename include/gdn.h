@@ -1,0 +1,133 @@
+/*
+ * gdn.h -- C ABI of libgdn: the Gated DeltaNet gated delta-rule recurrence on
+ * AMD MI355X (gfx950).
+ *
+ * The operation (paper, Section 3.2, display equations for old_v, delta, S';
+ * Section 2.2 for the decode / prefill split). For one sequence and one value
+ * head, with the recurrent state S stored as a d_v x d_k matrix:
+ *
+ *     S_t = alpha_t S_{t-1} (I - beta_t k_t k_t^T) + beta_t v_t k_t^T
+ *     o_t = S_t q_t                            (output from the updated state)
+ *     alpha_t = exp(g_t)
+ *
+ * g is passed as the LOG of the paper's multiplicative gate (g <= 0 in every
+ * intended use; positive g is accepted but can overflow inside the chunked
+ * form). beta is passed already activated, in [0, 1]. There is no q scale:
+ * callers fold 1/sqrt(d_k) into q.
+ *
+ * Grouped heads: HQK query/key heads and HV value heads with HV % HQK == 0;
+ * value head h reads query/key head h / (HV / HQK).
+ *
+ * Memory layouts (row-major, densely packed, element type per `dtype` for
+ * q/k/v/o, float32 for g, beta and states):
+ *   q, k            [T_total, HQK, DK]
+ *   v, o            [T_total, HV, DV]
+ *   g, beta         [T_total, HV]
+ *   cu_seqlens      [N + 1] int32: cu[0] = 0, non-decreasing, cu[N] = T_total
+ *   states          [N, HV, DV, DK]   ("k-last": the d_k index is contiguous)
+ *
+ * Ownership and execution: every pointer is DEVICE memory owned by the caller.
+ * The library never allocates, frees or retains memory; scratch space for
+ * prefill comes from the caller through `workspace` (destination-passing
+ * style, as in the paper's Sections 3.2 and 5.2). All work is enqueued on
+ * `stream` and returns without synchronising; cu_seqlens is never read on the
+ * host. The library holds no global state: calls are re-entrant, and calls on
+ * different streams are independent as long as their buffers do not overlap.
+ *
+ * Errors: argument validation happens on the host before any HIP call, so an
+ * invalid call enqueues nothing. Launch failures are reported as GDN_ERR_HIP.
+ * Device-side contract violations (cu_seqlens not non-decreasing, cu[N] !=
+ * T_total, overlapping in/out buffers other than the aliases allowed below)
+ * are undefined behaviour. NaN and Inf propagate without checks.
+ *
+ * Supported shapes: DK == DV in {32, 64, 128}; chunk in {16, 32, 64}.
+ */
+#ifndef GDN_H_
+#define GDN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gdn_status {
+  GDN_OK = 0,
+  GDN_ERR_INVALID_ARG = 1, /* null pointer, negative size, HV % HQK != 0 */
+  GDN_ERR_UNSUPPORTED = 2, /* head size / chunk size / dtype not built   */
+  GDN_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
+  GDN_ERR_HIP = 4          /* a HIP launch failed                        */
+} gdn_status;
+
+typedef enum gdn_dtype {
+  GDN_BF16 = 0, /* q, k, v, o are bfloat16; o is rounded to nearest even */
+  GDN_F32 = 1   /* q, k, v, o are float32                                 */
+} gdn_dtype;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *gdn_status_string(gdn_status status);
+
+/* Library version as major * 10000 + minor * 100 + patch. */
+int gdn_version(void);
+
+/*
+ * Bytes of device workspace gdn_prefill needs for these sizes (0 on invalid
+ * sizes). The bound depends on N and T_total only through ceil(T_total/chunk)
+ * + N, so a caller may size it once for the largest batch it will submit.
+ */
+size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
+                                  int32_t hqk, int32_t hv, int32_t dk,
+                                  int32_t dv, int32_t chunk);
+
+/*
+ * Chunked prefill over N packed variable-length sequences (paper, Sections
+ * 5.1, 5.2 and 5.5: the chunk / WY reformulation of the recurrence above).
+ *
+ * Each sequence is cut into chunks of `chunk` tokens starting at cu[n] (the
+ * last chunk of a sequence may be shorter). `chunk` changes only rounding,
+ * not the result. Per chunk, the intra-chunk recurrence is summarised by a
+ * unit lower-triangular WY factor; the state is carried chunk to chunk in
+ * float32.
+ *
+ *   q, k, v, g, beta, cu_seqlens : inputs, layouts above.
+ *   initial_state : [N, HV, DV, DK] float32, or NULL for zero states.
+ *   o             : [T_total, HV, DV] output (dtype as q).
+ *   final_state   : [N, HV, DV, DK] float32 output; may alias initial_state
+ *                   exactly (same pointer), in which case it is updated in
+ *                   place. A zero-length sequence yields its initial state.
+ *   workspace     : device scratch of at least gdn_prefill_workspace_size()
+ *                   bytes, 256-byte aligned; contents on entry are ignored.
+ *   stream        : HIP stream the work is enqueued on (NULL = default).
+ */
+gdn_status gdn_prefill(const void *q, const void *k, const void *v,
+                       const float *g, const float *beta,
+                       const int32_t *cu_seqlens, const float *initial_state,
+                       void *o, float *final_state, int32_t n_seqs,
+                       int64_t n_tokens, int32_t hqk, int32_t hv, int32_t dk,
+                       int32_t dv, int32_t chunk, gdn_dtype dtype,
+                       void *workspace, size_t workspace_bytes,
+                       hipStream_t stream);
+
+/*
+ * One decode step for a batch of B sequences, one token each (paper, Section
+ * 3.2: the one-pass form with the gate-scaled state; Section 5.4 for decode
+ * as a bandwidth/launch-shape problem). The state is read once and written
+ * once, in place.
+ *
+ *   q, k  : [B, HQK, DK]    v, o : [B, HV, DV]    g, beta : [B, HV]
+ *   state : [B, HV, DV, DK] float32, advanced in place.
+ */
+gdn_status gdn_decode(const void *q, const void *k, const void *v,
+                      const float *g, const float *beta, float *state,
+                      void *o, int32_t batch, int32_t hqk, int32_t hv,
+                      int32_t dk, int32_t dv, gdn_dtype dtype,
+                      hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GDN_H_ */

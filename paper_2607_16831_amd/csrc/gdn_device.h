@@ -1,0 +1,184 @@
+// gdn_device.h -- device-side helpers shared by the libgdn kernels (gfx950).
+//
+// Element types, bf16 packing, the 16x16x32 bf16 matrix-core instruction and
+// wave-level reductions. Nothing here depends on the recurrence itself.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gdn {
+
+constexpr int kWave = 64;  // CDNA wavefront width
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- bf16 bits
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
+  __bf16 b = (__bf16)x;  // v_cvt_pk_bf16_f32: round to nearest even
+  return __builtin_bit_cast(uint16_t, b);
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16_bits(lo) | ((uint32_t)f32_to_bf16_bits(hi) << 16);
+}
+
+// Eight consecutive elements of a row, returned as packed bf16 (16 bytes).
+// bf16 input is copied bit-exactly; f32 input is rounded to nearest even.
+template <typename T>
+struct Elem;
+
+template <>
+struct Elem<__bf16> {
+  static __device__ __forceinline__ uint4 load8(const __bf16 *p) {
+    return *reinterpret_cast<const uint4 *>(p);
+  }
+  static __device__ __forceinline__ float load1(const __bf16 *p) {
+    return bf16_bits_to_f32(*reinterpret_cast<const uint16_t *>(p));
+  }
+  static __device__ __forceinline__ void load4(const __bf16 *p, float out[4]) {
+    uint2 r = *reinterpret_cast<const uint2 *>(p);
+    out[0] = bf16_bits_to_f32(r.x & 0xffffu);
+    out[1] = bf16_bits_to_f32(r.x >> 16);
+    out[2] = bf16_bits_to_f32(r.y & 0xffffu);
+    out[3] = bf16_bits_to_f32(r.y >> 16);
+  }
+  static __device__ __forceinline__ void store1(__bf16 *p, float x) {
+    *reinterpret_cast<uint16_t *>(p) = f32_to_bf16_bits(x);
+  }
+};
+
+template <>
+struct Elem<float> {
+  static __device__ __forceinline__ uint4 load8(const float *p) {
+    float4 a = reinterpret_cast<const float4 *>(p)[0];
+    float4 b = reinterpret_cast<const float4 *>(p)[1];
+    return make_uint4(pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w),
+                      pack_bf16x2(b.x, b.y), pack_bf16x2(b.z, b.w));
+  }
+  static __device__ __forceinline__ float load1(const float *p) { return *p; }
+  static __device__ __forceinline__ void load4(const float *p, float out[4]) {
+    float4 r = *reinterpret_cast<const float4 *>(p);
+    out[0] = r.x;
+    out[1] = r.y;
+    out[2] = r.z;
+    out[3] = r.w;
+  }
+  static __device__ __forceinline__ void store1(float *p, float x) { *p = x; }
+};
+
+// ---------------------------------------------------------------- MFMA
+// v_mfma_f32_16x16x32_bf16, one wavefront:
+//   A (16 x 32): lane l supplies row (l % 16), contraction slots 8*(l/16)+[0,8)
+//   B (32 x 16): lane l supplies column (l % 16), the same contraction slots
+//   D (16 x 16): lane l receives column (l % 16), rows 4*(l/16)+[0,4)
+// A and B name contraction slots identically, so any assignment of true
+// contraction indices to slots is valid as long as both operands use it.
+__device__ __forceinline__ f32x4 mfma_16x16x32(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+      __builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// v_mfma_f32_16x16x4_f32, one wavefront:
+//   A (16 x 4): lane l supplies A[l % 16][l / 16]
+//   B (4 x 16): lane l supplies B[l / 16][l % 16]
+//   D: as above. Four of these cover a 16 x 16 x 16 product; in step kk,
+//   contraction slot g stands for index 4 g + kk, so a B operand can be taken
+//   straight from a lane's own accumulator element kk.
+__device__ __forceinline__ f32x4 mfma_16x16x4_f32(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------- buffers
+// Raw buffer resources: a base address and byte extent held in scalar
+// registers, addressed with a 32-bit per-lane byte offset. Reads past the
+// extent return zero and writes past it are dropped by the hardware; partial
+// chunks rely on this instead of branches.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcWord3 = 0x00020000;  // raw (untyped) buffer, gfx9 family
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0,
+                                           (int)bytes, kRsrcWord3);
+}
+__device__ __forceinline__ uint4 buf_load_b128(rsrc_t r, uint32_t off) {
+  const auto x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return make_uint4(x[0], x[1], x[2], x[3]);
+}
+__device__ __forceinline__ float buf_load_f32(rsrc_t r, uint32_t off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ __forceinline__ float4 buf_load_f32x4(rsrc_t r, uint32_t off) {
+  const uint4 x = buf_load_b128(r, off);
+  return make_float4(__uint_as_float(x.x), __uint_as_float(x.y),
+                     __uint_as_float(x.z), __uint_as_float(x.w));
+}
+
+// Element access through a buffer resource; offsets are in elements.
+template <typename T>
+struct BufElem;
+
+template <>
+struct BufElem<__bf16> {
+  static __device__ __forceinline__ uint4 load8(rsrc_t r, uint32_t e) {
+    return buf_load_b128(r, e * 2u);
+  }
+  static __device__ __forceinline__ float load1(rsrc_t r, uint32_t e) {
+    return bf16_bits_to_f32(__builtin_amdgcn_raw_buffer_load_b16(r, e * 2u, 0, 0));
+  }
+  static __device__ __forceinline__ void store1(rsrc_t r, uint32_t e, float x) {
+    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_bits(x), r, e * 2u, 0, 0);
+  }
+};
+
+template <>
+struct BufElem<float> {
+  static __device__ __forceinline__ uint4 load8(rsrc_t r, uint32_t e) {
+    const float4 a = buf_load_f32x4(r, e * 4u), b = buf_load_f32x4(r, e * 4u + 16u);
+    return make_uint4(pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w),
+                      pack_bf16x2(b.x, b.y), pack_bf16x2(b.z, b.w));
+  }
+  static __device__ __forceinline__ float load1(rsrc_t r, uint32_t e) {
+    return buf_load_f32(r, e * 4u);
+  }
+  static __device__ __forceinline__ void store1(rsrc_t r, uint32_t e, float x) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, e * 4u, 0, 0);
+  }
+};
+
+// ---------------------------------------------------------------- reductions
+// Sum over aligned groups of `W` consecutive lanes (W a power of two <= 64).
+template <int W>
+__device__ __forceinline__ float group_sum(float x) {
+#pragma unroll
+  for (int m = W / 2; m >= 1; m >>= 1) x += __shfl_xor(x, m, kWave);
+  return x;
+}
+
+// ---------------------------------------------------------------- barriers
+// Work-group barrier that orders LDS traffic only. Unlike __syncthreads() it
+// does not wait for outstanding global loads and stores, so prefetches stay
+// in flight across it; the memory clobber keeps the compiler from moving
+// memory accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Orders LDS accesses of one wavefront for the compiler. The hardware already
+// executes a wavefront's LDS instructions in issue order, so data written by
+// one lane is visible to other lanes of the same wavefront afterwards.
+__device__ __forceinline__ void wave_lds_fence() { asm volatile("" ::: "memory"); }
+
+// ---------------------------------------------------------------- streaming
+__device__ __forceinline__ f32x4 load_stream(const float *p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(p));
+}
+__device__ __forceinline__ void store_stream(float *p, f32x4 x) {
+  __builtin_nontemporal_store(x, reinterpret_cast<f32x4 *>(p));
+}
+
+}  // namespace gdn

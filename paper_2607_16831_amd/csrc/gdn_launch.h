@@ -1,0 +1,61 @@
+// gdn_launch.h -- internal interface between the C ABI layer and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/gdn.h"
+
+namespace gdn {
+
+struct DecodeArgs {
+  const void *q, *k, *v;
+  const float *g, *beta;
+  float *state;
+  void *o;
+  int batch, hqk, hv, d;
+  gdn_dtype dtype;
+  hipStream_t stream;
+};
+
+struct PrefillArgs {
+  const void *q, *k, *v;
+  const float *g, *beta;
+  const int32_t *cu_seqlens;
+  const float *initial_state;
+  void *o;
+  float *final_state;
+  int n_seqs;
+  int64_t n_tokens;
+  int hqk, hv, d, chunk;
+  gdn_dtype dtype;
+  void *workspace;
+  hipStream_t stream;
+};
+
+// Device workspace carved out of the caller's buffer (all offsets 256-aligned).
+struct PrefillWorkspace {
+  size_t chunk_off;   // int32 [N + 1]: first global chunk index of each sequence
+  size_t gamma;       // f32  [chunks, HV, C]: in-chunk cumulative log-decay
+  size_t tfrag;       // bf16 [chunks, HV, FRAG]: (I + A)^-1 in operand order
+  size_t pfrag;       // bf16 [chunks, HV, FRAG]: decay-masked Q K^T, same order
+  size_t total;
+};
+
+// Elements of one C x C matrix stored as 16x16x32 A-operand fragments.
+inline int64_t frag_elems(int chunk) {
+  const int nib = chunk / 16;
+  const int ks = (chunk + 31) / 32;
+  return (int64_t)nib * ks * 64 * 8;
+}
+inline int64_t chunk_bound(int n_seqs, int64_t n_tokens, int chunk) {
+  return (n_tokens + chunk - 1) / chunk + n_seqs;
+}
+PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hv,
+                                          int chunk);
+
+hipError_t launch_decode(const DecodeArgs &a);
+hipError_t launch_prefill(const PrefillArgs &a, const PrefillWorkspace &ws);
+
+}  // namespace gdn

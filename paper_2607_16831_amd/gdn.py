@@ -1,0 +1,174 @@
+"""ctypes binding for libgdn (C ABI in include/gdn.h).
+
+Argument marshalling only: every step of prefill and decode runs in the HIP
+kernels of ``libgdn.so``. PyTorch supplies device memory and the current HIP
+stream. If the library has not been built, or the tensors are not on a GPU,
+calls raise -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgdn.so")
+
+GDN_OK, GDN_ERR_INVALID_ARG, GDN_ERR_UNSUPPORTED, GDN_ERR_WORKSPACE, GDN_ERR_HIP = range(5)
+GDN_BF16, GDN_F32 = 0, 1
+
+EXPORTS = ("gdn_status_string", "gdn_version", "gdn_prefill_workspace_size",
+           "gdn_prefill", "gdn_decode")
+
+_lib = None
+
+
+class GdnError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__("%s failed: %s (status %d)" % (fn, status_string(status), status))
+
+
+def lib() -> ctypes.CDLL:
+    """Load libgdn.so from the package directory (raises if it is missing)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                "libgdn.so is not built (%s); run python -m paper_2607_16831_amd.build"
+                % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        vp, fp, ip = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p
+        i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        L.gdn_status_string.argtypes = [ctypes.c_int]
+        L.gdn_status_string.restype = ctypes.c_char_p
+        L.gdn_version.argtypes = []
+        L.gdn_version.restype = ctypes.c_int
+        L.gdn_prefill_workspace_size.argtypes = [i32, i64, i32, i32, i32, i32, i32]
+        L.gdn_prefill_workspace_size.restype = sz
+        L.gdn_prefill.argtypes = [vp, vp, vp, fp, fp, ip, fp, vp, fp, i32, i64,
+                                  i32, i32, i32, i32, i32, ctypes.c_int, vp, sz, vp]
+        L.gdn_prefill.restype = ctypes.c_int
+        L.gdn_decode.argtypes = [vp, vp, vp, fp, fp, fp, vp, i32, i32, i32, i32,
+                                 i32, ctypes.c_int, vp]
+        L.gdn_decode.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().gdn_status_string(int(status)).decode()
+
+
+def version() -> int:
+    return int(lib().gdn_version())
+
+
+def prefill_workspace_size(n_seqs, n_tokens, hqk, hv, dk, dv, chunk) -> int:
+    return int(lib().gdn_prefill_workspace_size(n_seqs, n_tokens, hqk, hv, dk, dv, chunk))
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return GDN_BF16
+    if t.dtype == torch.float32:
+        return GDN_F32
+    raise TypeError("q/k/v must be bfloat16 or float32, got %s" % t.dtype)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check_dev(*ts):
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError("libgdn takes device tensors (got a %s tensor)" % t.device)
+        if not t.is_contiguous():
+            raise ValueError("libgdn takes contiguous tensors")
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def prefill_raw(q, k, v, g, beta, cu_seqlens, initial_state, o, final_state,
+                n_seqs, n_tokens, hqk, hv, dk, dv, chunk, dtype, workspace,
+                workspace_bytes, stream) -> int:
+    """Direct call of gdn_prefill with integer pointers; returns the status."""
+    return int(lib().gdn_prefill(q, k, v, g, beta, cu_seqlens, initial_state, o,
+                                 final_state, n_seqs, n_tokens, hqk, hv, dk, dv,
+                                 chunk, dtype, workspace, workspace_bytes, stream))
+
+
+def decode_raw(q, k, v, g, beta, state, o, batch, hqk, hv, dk, dv, dtype,
+               stream) -> int:
+    """Direct call of gdn_decode with integer pointers; returns the status."""
+    return int(lib().gdn_decode(q, k, v, g, beta, state, o, batch, hqk, hv, dk,
+                                dv, dtype, stream))
+
+
+def alloc_workspace(n_seqs, n_tokens, hqk, hv, d, chunk, device) -> torch.Tensor:
+    nbytes = prefill_workspace_size(n_seqs, n_tokens, hqk, hv, d, d, chunk)
+    if nbytes == 0:
+        raise ValueError("unsupported prefill sizes")
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor,
+            beta: torch.Tensor, cu_seqlens: torch.Tensor,
+            initial_state: Optional[torch.Tensor] = None, chunk: int = 64,
+            o: Optional[torch.Tensor] = None,
+            final_state: Optional[torch.Tensor] = None,
+            workspace: Optional[torch.Tensor] = None,
+            stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Chunked prefill; returns (o [T, HV, DV], final_state [N, HV, DV, DK])."""
+    T, hqk, dk = q.shape
+    hv, dv = v.shape[1], v.shape[2]
+    N = cu_seqlens.shape[0] - 1
+    if o is None:
+        o = torch.empty((T, hv, dv), dtype=q.dtype, device=q.device)
+    if final_state is None:
+        final_state = torch.empty((N, hv, dv, dk), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = alloc_workspace(N, T, hqk, hv, dk, chunk, q.device)
+    _check_dev(q, k, v, g, beta, cu_seqlens, initial_state, o, final_state, workspace)
+    if cu_seqlens.dtype != torch.int32:
+        raise TypeError("cu_seqlens must be int32")
+    if g.dtype != torch.float32 or beta.dtype != torch.float32:
+        raise TypeError("g and beta must be float32")
+    if k.dtype != q.dtype or v.dtype != q.dtype or o.dtype != q.dtype:
+        raise TypeError("q, k, v and o must share one dtype")
+    st = prefill_raw(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(cu_seqlens),
+                     _ptr(initial_state), _ptr(o), _ptr(final_state), N, T, hqk, hv,
+                     dk, dv, chunk, _dtype_code(q), _ptr(workspace),
+                     workspace.numel(), _stream(stream))
+    if st != GDN_OK:
+        raise GdnError("gdn_prefill", st)
+    return o, final_state
+
+
+def decode(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor,
+           beta: torch.Tensor, state: torch.Tensor,
+           o: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """One decode step; advances ``state`` in place and returns o [B, HV, DV]."""
+    B, hqk, dk = q.shape
+    hv, dv = v.shape[1], v.shape[2]
+    if o is None:
+        o = torch.empty((B, hv, dv), dtype=q.dtype, device=q.device)
+    _check_dev(q, k, v, g, beta, state, o)
+    if g.dtype != torch.float32 or beta.dtype != torch.float32 or state.dtype != torch.float32:
+        raise TypeError("g, beta and state must be float32")
+    if k.dtype != q.dtype or v.dtype != q.dtype or o.dtype != q.dtype:
+        raise TypeError("q, k, v and o must share one dtype")
+    st = decode_raw(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(state),
+                    _ptr(o), B, hqk, hv, dk, dv, _dtype_code(q), _stream(stream))
+    if st != GDN_OK:
+        raise GdnError("gdn_decode", st)
+    return o

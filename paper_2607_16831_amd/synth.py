@@ -18,8 +18,9 @@ contest's 54 decode and 100 prefill workloads):
 * q, k, v are produced in fp32 and rounded to bf16 (round to nearest even)
   when the workload is bf16; g, beta and states stay fp32.
 
-One numpy PCG64 stream per workload, seeded explicitly; draw order: sequence
-lengths, q, k, v, g noise, beta noise, initial state.
+One seeded torch CPU generator per workload (deterministic for a given seed
+and torch build); draw order: sequence lengths, q, k, v, g noise, beta noise,
+initial state. Arithmetic on the draws is fp32.
 """
 from __future__ import annotations
 
@@ -73,33 +74,24 @@ WORKLOADS = {w.name: w for w in
               PREFILL_LONG)}
 
 
-def _unit_rows(x: np.ndarray) -> np.ndarray:
-    n = np.sqrt(np.sum(x.astype(np.float64) ** 2, axis=-1, keepdims=True))
-    return (x / np.maximum(n, 1e-30)).astype(np.float32)
+def _unit_rows(x: torch.Tensor) -> torch.Tensor:
+    return x / torch.linalg.vector_norm(x, dim=-1, keepdim=True).clamp_min(1e-30)
 
 
-def _softplus(x: np.ndarray) -> np.ndarray:
-    return np.logaddexp(0.0, x.astype(np.float64))
+def _cast(x: torch.Tensor, dtype: str) -> torch.Tensor:
+    x = x.contiguous()
+    return x.to(torch.bfloat16) if dtype == "bf16" else x
 
 
-def _sigmoid(x: np.ndarray) -> np.ndarray:
-    return 1.0 / (1.0 + np.exp(-x.astype(np.float64)))
-
-
-def _to_torch(x: np.ndarray, dtype: str) -> torch.Tensor:
-    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
-    return t.to(torch.bfloat16) if dtype == "bf16" else t
-
-
-def seq_lengths(w: Workload, rng: Optional[np.random.Generator] = None):
+def seq_lengths(w: Workload, gen: Optional[torch.Generator] = None):
     if w.lengths is not None:
         return np.asarray(w.lengths, dtype=np.int64)
     if w.seq_len is not None:
         return np.full(w.n_seqs, w.seq_len, dtype=np.int64)
     if w.len_range is not None:
-        assert rng is not None
+        assert gen is not None
         lo, hi = w.len_range
-        return rng.integers(lo, hi + 1, size=w.n_seqs).astype(np.int64)
+        return torch.randint(lo, hi + 1, (w.n_seqs,), generator=gen).numpy().astype(np.int64)
     if w.kind == "decode":
         return np.ones(w.n_seqs, dtype=np.int64)
     raise ValueError("workload %s has no length rule" % w.name)
@@ -109,37 +101,30 @@ def make(w: Workload, seed: Optional[int] = None) -> dict:
     """Draw one input set for workload ``w`` as CPU torch tensors.
 
     Returns a dict with q, k, v (bf16 or f32), g, beta (f32), cu_seqlens
-    (int32, prefill only), initial_state (f32 or None; for decode the state
-    that is advanced in place) and the workload itself under "w".
+    (int32), initial_state (f32 or None; for decode the state that is
+    advanced in place) and the workload itself under "w".
     """
-    rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
-    lens = seq_lengths(w, rng)
+    gen = torch.Generator().manual_seed(w.seed if seed is None else seed)
+    lens = seq_lengths(w, gen)
     T = int(lens.sum())
     d = w.d
-    q = _unit_rows(rng.standard_normal((T, w.hqk, d), dtype=np.float32))
-    q = (q / np.float32(np.sqrt(d))).astype(np.float32)
-    k = _unit_rows(rng.standard_normal((T, w.hqk, d), dtype=np.float32))
-    v = rng.standard_normal((T, w.hv, d), dtype=np.float32)
-    gz = rng.standard_normal((T, w.hv), dtype=np.float32)
-    bz = rng.standard_normal((T, w.hv), dtype=np.float32)
+    q = _unit_rows(torch.randn((T, w.hqk, d), generator=gen)) / float(np.sqrt(d))
+    k = _unit_rows(torch.randn((T, w.hqk, d), generator=gen))
+    v = torch.randn((T, w.hv, d), generator=gen)
+    gz = torch.randn((T, w.hv), generator=gen)
+    bz = torch.randn((T, w.hv), generator=gen)
     if w.g_zero:
-        g = np.zeros((T, w.hv), dtype=np.float32)
+        g = torch.zeros((T, w.hv))
     else:
-        g = (-w.g_scale * _softplus(gz + np.float32(w.g_mu))).astype(np.float32)
-    beta = _sigmoid(bz).astype(np.float32)
-    n_states = w.n_seqs
+        g = -w.g_scale * torch.nn.functional.softplus(gz + w.g_mu)
+    beta = torch.sigmoid(bz)
     s0 = None
     if w.state_std > 0:
-        s0 = (w.state_std * rng.standard_normal((n_states, w.hv, d, d),
-                                                dtype=np.float32))
-        s0 = torch.from_numpy(s0.astype(np.float32))
+        s0 = w.state_std * torch.randn((w.n_seqs, w.hv, d, d), generator=gen)
+    elif w.kind == "decode":
+        s0 = torch.zeros((w.n_seqs, w.hv, d, d))
     cu = np.zeros(w.n_seqs + 1, dtype=np.int32)
     cu[1:] = np.cumsum(lens)
-    out = dict(w=w, q=_to_torch(q, w.dtype), k=_to_torch(k, w.dtype),
-               v=_to_torch(v, w.dtype), g=torch.from_numpy(g),
-               beta=torch.from_numpy(beta), initial_state=s0,
-               cu_seqlens=torch.from_numpy(cu))
-    if w.kind == "decode":
-        if s0 is None:
-            out["initial_state"] = torch.zeros(w.n_seqs, w.hv, d, d)
-    return out
+    return dict(w=w, q=_cast(q, w.dtype), k=_cast(k, w.dtype), v=_cast(v, w.dtype),
+                g=g.float().contiguous(), beta=beta.float().contiguous(),
+                initial_state=s0, cu_seqlens=torch.from_numpy(cu))

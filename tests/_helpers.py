@@ -1,0 +1,45 @@
+"""Shared test helpers: error metrics, GPU staging, oracle slicing."""
+import numpy as np
+import torch
+
+# Parity bars (rel-L2 against the fp64 oracle): bf16 outputs and fp32 state.
+O_BAR = 2e-2
+STATE_BAR = 5e-3
+
+
+def rel_l2(x, y) -> float:
+    """||x - y||_2 / ||y||_2 in fp64 over the whole tensor (y = reference)."""
+    x = x.detach().cpu().double().numpy() if hasattr(x, "detach") else np.asarray(x, np.float64)
+    y = y.detach().cpu().double().numpy() if hasattr(y, "detach") else np.asarray(y, np.float64)
+    ny = np.linalg.norm(y)
+    if ny == 0:
+        return float(np.linalg.norm(x))
+    return float(np.linalg.norm(x - y) / ny)
+
+
+def require_gpu():
+    if not torch.cuda.is_available():
+        raise RuntimeError("GPU test run without a visible GPU")
+    return torch.device("cuda:0")
+
+
+def to_dev(x: dict, dev):
+    out = {}
+    for k, v in x.items():
+        out[k] = v.to(dev).contiguous() if isinstance(v, torch.Tensor) else v
+    return out
+
+
+def chain_slice(x: dict, n: int, h: int):
+    """Inputs of one (sequence, value head) chain as a 1-head oracle problem."""
+    w = x["w"]
+    grp = w.hv // w.hqk
+    cu = x["cu_seqlens"].numpy()
+    t0, t1 = int(cu[n]), int(cu[n + 1])
+    hk = h // grp
+    s0 = x["initial_state"]
+    return dict(q=x["q"][t0:t1, hk:hk + 1], k=x["k"][t0:t1, hk:hk + 1],
+                v=x["v"][t0:t1, h:h + 1], g=x["g"][t0:t1, h:h + 1],
+                beta=x["beta"][t0:t1, h:h + 1],
+                cu_seqlens=np.array([0, t1 - t0], np.int32),
+                initial_state=None if s0 is None else s0[n:n + 1, h:h + 1])
