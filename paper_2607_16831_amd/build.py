@@ -21,6 +21,9 @@ HIPCC_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", "--offload-arch=" + ARCH,
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-fno-gpu-rdc", "-Wall", "-Wno-unused-function",
+    # matrix-core accumulators in ordinary VGPRs: no copies between the
+    # accumulation registers and the VGPRs the vector ALU reads
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

@@ -37,7 +37,7 @@ struct PrefillArgs {
 // Device workspace carved out of the caller's buffer (all offsets 256-aligned).
 struct PrefillWorkspace {
   size_t chunk_off;   // int32 [N + 1]: first global chunk index of each sequence
-  size_t gamma;       // f32  [chunks, HV, C]: in-chunk cumulative log-decay
+  size_t decay;       // f32  [chunks, HV, 2, C]: exp(gamma_i), exp(gamma_last - gamma_i)
   size_t tfrag;       // bf16 [chunks, HV, FRAG]: (I + A)^-1 in operand order
   size_t pfrag;       // bf16 [chunks, HV, FRAG]: decay-masked Q K^T, same order
   size_t total;

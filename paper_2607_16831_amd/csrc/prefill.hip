@@ -123,7 +123,7 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k,
     const float *__restrict__ g, const float *__restrict__ beta,
     const int32_t *__restrict__ cu, const int32_t *__restrict__ off,
-    int n_seqs, int hqk, int hv, int group, float *__restrict__ gam_ws,
+    int n_seqs, int hqk, int hv, int group, float *__restrict__ dec_ws,
     uint16_t *__restrict__ tfrag, uint16_t *__restrict__ pfrag) {
   using F = Cfg<D, C>;
   constexpr int NIB = F::NIB, KS = F::KS;
@@ -211,7 +211,12 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
       const float y = __shfl_up(gam, d, 64);
       if (lane >= d) gam += y;
     }
-    if (wave == 0 && lane < C) gam_ws[slot * C + lane] = gam;
+    const float glast = __shfl(gam, C - 1, 64);
+    if (wave == 0 && lane < C) {
+      // decay factors for the carry: exp(gamma_i) and exp(gamma_last - gamma_i)
+      dec_ws[slot * 2 * C + lane] = __expf(gam);
+      dec_ws[slot * 2 * C + C + lane] = __expf(glast - gam);
+    }
 
     f32x4 At[NIB], Z[NIB];
 #pragma unroll
@@ -327,7 +332,15 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
           Zc = mfma_16x16x4_f32(L.u.inv.linv[c][l16 * 17 + 4 * g4 + kk], R[kk], Zc);
         Z[c] = -Zc;
       }
-      // T as A-operand fragments, same token order as P.
+      // Fold beta into the factor: the carry uses T' = T diag(beta), so that
+      // U = T' (V - exp(gamma) X) needs no beta of its own.
+#pragma unroll
+      for (int c = 0; c < NIB; ++c) {
+        if (c > ib) continue;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Z[c][e] *= __shfl(bta, 16 * c + 4 * g4 + e, 64);
+      }
+      // T' as A-operand fragments, same token order as P.
       uint16_t *tf = tfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
@@ -343,108 +356,134 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
 }
 
 // ============================================================ chunk carry
-// One work-group per (sequence, value head, 16-row value tile); wavefront w
-// owns token block w of the chunk and key tiles w, w + 4 of the state. All
-// global reads go through buffer resources rebuilt per chunk from scalars, so
-// the per-lane offsets are loop invariant and rows past the end of the
-// sequence read as zero (they then contribute exact zeros: beta = 0 there).
+// One work-group of 8 wavefronts per (sequence, value head, 16-row value
+// tile), two wavefronts per SIMD. Wavefronts 0-3 own token block w of the
+// chunk for X = K S^T, Y and U = T Y; wavefronts 4-7 own token block w - 4 for
+// Q S^T and O; all eight update one 16-key tile of the state each. The next
+// chunk is prefetched into registers while the current one is computed; K and
+// Q go through row-major LDS tiles (16-byte chunks XOR-swizzled by row) and
+// K^T is read from the same tile with the LDS transpose load.
+//
+// All global reads go through buffer resources rebuilt per chunk from
+// scalars, so per-lane offsets are loop invariant and rows past the end of
+// the sequence read as zero (beta is zero there, so they contribute exact
+// zeros); stores past the end are dropped by the resource extent.
+template <int D, int C, typename TIn = __bf16>
+struct CarryCfg {
+  using F = Cfg<D, C>;
+  static constexpr int NT = 512;                      // threads
+  static constexpr int NP = C * (D / 8);              // 16-byte pieces of K (or Q)
+  // Wavefronts 0-3 fetch K, wavefronts 4-7 fetch Q: KP pieces per thread.
+  static constexpr int KP = (NP + NT / 2 - 1) / (NT / 2);
+  // Per-chunk small data, fetched by the first threads: the 16-value V tile
+  // of every token (VPR 16-byte pieces per token) and the 2C decay factors.
+  static constexpr int VPR = (16 * (int)sizeof(TIn)) / 16;
+  static constexpr int VP = C * VPR;
+  static constexpr int SP = VP + (2 * C) / 4;
+  static_assert(SP <= NT, "small data fits one piece per thread");
+};
+
 template <int D, int C>
 struct ChunkRegs {
   using F = Cfg<D, C>;
-  uint4 kr[4];       // K piece: rows 4 rg + [0, 4), columns 8 cg + [0, 8)
-  uint4 qa[F::DS];   // Q rows as the A operand of Q S^T
-  uint4 ta[F::KS];   // T fragments of this wave's token block
-  uint4 pa[F::KS];   // P fragments of this wave's token block
-  float vv[4], bb[4];
-  float4 gg;
-  float glast;
+  uint4 kq[CarryCfg<D, C>::KP];   // K pieces (waves 0-3) or Q pieces (4-7)
+  uint4 fa[F::KS];   // T' fragments (waves 0-3) or P fragments (waves 4-7)
+  uint4 sd;          // one piece of the V tile or of the decay factors
 };
 
-// Per-lane element offsets, fixed for the whole sequence.
+// Per-lane offsets, fixed for the whole sequence.
+template <int KP>
 struct CarryLane {
-  uint32_t k, q, v, b, frag, gam;
+  uint32_t kq[KP];   // elements
+  uint32_t frag;     // elements
+  uint32_t sd;       // bytes, into V (sd_v) or the decay row
+  bool sd_v, sd_any;
 };
 
 template <int D, int C, typename TIn>
 __device__ __forceinline__ void carry_fetch(
-    ChunkRegs<D, C> &r, const CarryLane &ln, const TIn *__restrict__ q,
-    const TIn *__restrict__ k, const TIn *__restrict__ v,
-    const float *__restrict__ beta, const float *__restrict__ gam_ws,
+    ChunkRegs<D, C> &r, const CarryLane<CarryCfg<D, C>::KP> &ln, bool tgroup,
+    const TIn *__restrict__ q, const TIn *__restrict__ k,
+    const TIn *__restrict__ v, const float *__restrict__ dec_ws,
     const uint16_t *__restrict__ tfrag, const uint16_t *__restrict__ pfrag,
-    int64_t t0, int nvalid, int64_t slot, int h, int hk, int hqk, int hv, int v0) {
+    int64_t t0, int nvalid, int64_t slot, int h, int hk, int hqk, int hv,
+    int v0) {
   using F = Cfg<D, C>;
-  const uint32_t kb = (uint32_t)(nvalid * hqk * D * sizeof(TIn));
-  const rsrc_t rk = make_rsrc(k + (t0 * hqk + hk) * D, kb);
-  const rsrc_t rq = make_rsrc(q + (t0 * hqk + hk) * D, kb);
-  const rsrc_t rv = make_rsrc(v + (t0 * hv + h) * D + v0, (uint32_t)(nvalid * hv * D * sizeof(TIn)));
-  const rsrc_t rb = make_rsrc(beta + t0 * hv + h, (uint32_t)(nvalid * hv * 4));
-  const rsrc_t rt = make_rsrc(tfrag + slot * F::FRAG, F::FRAG * 2);
-  const rsrc_t rp = make_rsrc(pfrag + slot * F::FRAG, F::FRAG * 2);
-  const rsrc_t rg = make_rsrc(gam_ws + slot * C, C * 4);
+  const rsrc_t rkq = make_rsrc((tgroup ? k : q) + (t0 * hqk + hk) * D,
+                               (uint32_t)(nvalid * hqk * D * sizeof(TIn)));
+  const rsrc_t rf = make_rsrc((tgroup ? tfrag : pfrag) + slot * F::FRAG, F::FRAG * 2);
 #pragma unroll
-  for (int rr = 0; rr < 4; ++rr)
-    r.kr[rr] = BufElem<TIn>::load8(rk, ln.k + (uint32_t)(rr * hqk * D));
+  for (int u = 0; u < CarryCfg<D, C>::KP; ++u) r.kq[u] = BufElem<TIn>::load8(rkq, ln.kq[u]);
 #pragma unroll
-  for (int s = 0; s < F::DS; ++s) r.qa[s] = BufElem<TIn>::load8(rq, ln.q + 32 * s);
-#pragma unroll
-  for (int s = 0; s < F::KS; ++s) {
-    r.ta[s] = buf_load_b128(rt, (ln.frag + s * 512) * 2);
-    r.pa[s] = buf_load_b128(rp, (ln.frag + s * 512) * 2);
+  for (int s = 0; s < F::KS; ++s) r.fa[s] = buf_load_b128(rf, (ln.frag + s * 512) * 2);
+  if (ln.sd_any) {
+    const rsrc_t rs = ln.sd_v
+        ? make_rsrc(v + (t0 * hv + h) * D + v0, (uint32_t)(nvalid * hv * D * sizeof(TIn)))
+        : make_rsrc(dec_ws + slot * 2 * C, 2 * C * 4);
+    r.sd = buf_load_b128(rs, ln.sd);
   }
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    r.vv[e] = BufElem<TIn>::load1(rv, ln.v + (uint32_t)(e * hv * D));
-    r.bb[e] = buf_load_f32(rb, (ln.b + (uint32_t)(e * hv)) * 4);
-  }
-  r.gg = buf_load_f32x4(rg, ln.gam * 4);
-  r.glast = buf_load_f32(rg, (C - 1) * 4);
 }
 
-template <int D, int C>
+template <int D, int C, typename TIn>
 struct CarryLds {
   using F = Cfg<D, C>;
-  uint16_t Kn[2][C * D];        // K chunk, row-major, 16-byte chunks swizzled
-  uint16_t Kt[2][D * F::CP];    // K chunk transposed, tokens in tok_pos order
+  uint16_t Kn[2][F::CP * D];    // K chunk, row-major, swizzled (double buffered);
+                                // rows C..CP-1 stay zero for chunks below 32
+  uint16_t Qn[C * D];           // Q chunk, same layout (read before the first
+                                // barrier of a chunk, refilled after it)
+  TIn Vl[2][16][C + 8];         // V tile, [value][token], input element type
+  float Dl[2][2 * C];           // exp(gamma_i), then exp(gamma_last - gamma_i)
   uint16_t Sl[16 * F::LDK];     // bf16 copy of the state tile, [value][key]
   uint16_t Yl[16 * F::LDV];     // Y,  [value][token position]
   uint16_t Ul[16 * F::LDV];     // U,  [value][token position]
   uint16_t Uh[16 * F::LDV];     // exp(gamma_last - gamma) U, same layout
+  uint32_t Ol[4][16 * 16 * 4 / 4];  // per-wavefront output staging (fp32 worst case)
 };
 
-// 16-byte chunk swizzles (XOR with a row function), chosen so that both the
-// 16-lane write pattern of the K commit and the 16-lane read pattern of the
-// matrix operands touch 16 distinct bank groups.
+// Element index of (row, column) in a swizzled row-major [C][D] tile: 16-byte
+// chunks are XORed with a row function so that both 16 consecutive rows at
+// one column (matrix-operand reads) and 16 chunks of one row (the commit)
+// fall on distinct bank groups.
 template <int D>
-__device__ __forceinline__ int kn_index(int row, int chunk) {
+__device__ __forceinline__ int kn_index(int row, int col) {
   const int sw = ((row & 15) ^ ((row >> 4) & 3)) & (D / 8 - 1);
-  return row * D + 8 * (chunk ^ sw);
-}
-template <int CP>
-__device__ __forceinline__ int kt_index(int row, int chunk) {
-  const int sw = (row >> 1) & (CP / 8 - 1);
-  return row * CP + 8 * (chunk ^ sw);
+  return row * D + 8 * ((col >> 3) ^ sw) + (col & 7);
 }
 
-// Write a K piece into the row-major tile and the transposed tile.
+// Pieces p = tid4 + 256 u of K (waves 0-3) or Q (waves 4-7), tid4 = tid % 256.
 template <int D, int C>
-__device__ __forceinline__ void carry_commit_k(const ChunkRegs<D, C> &r,
-                                               uint16_t *Kn, uint16_t *Kt,
-                                               int tid) {
-  using F = Cfg<D, C>;
-  if (tid >= F::PIECES) return;
-  const int rg = tid % (C / 4), cg = tid / (C / 4);
+__device__ __forceinline__ void carry_commit(const ChunkRegs<D, C> &r,
+                                             uint16_t *dst, int tid4) {
+  using CC = CarryCfg<D, C>;
 #pragma unroll
-  for (int rr = 0; rr < 4; ++rr)
-    *reinterpret_cast<uint4 *>(&Kn[kn_index<D>(4 * rg + rr, cg)]) = r.kr[rr];
-  const int p = tok_pos(4 * rg);
+  for (int u = 0; u < CC::KP; ++u) {
+    const int p = tid4 + (CC::NT / 2) * u;
+    if (CC::NP % (CC::NT / 2) != 0 && p >= CC::NP) continue;
+    *reinterpret_cast<uint4 *>(&dst[kn_index<D>(p / (D / 8), 8 * (p % (D / 8)))]) = r.kq[u];
+  }
+}
+
+// Small-data piece p of the thread: V pieces go to the [value][token] tile,
+// decay quads to their row.
+template <int D, int C, typename TIn>
+__device__ __forceinline__ void carry_commit_small(const ChunkRegs<D, C> &r,
+                                                   TIn (*Vl)[C + 8], float *Dl,
+                                                   int p) {
+  using CC = CarryCfg<D, C, TIn>;
+  if (p < CC::VP) {
+    const int tok = p / CC::VPR, part = p % CC::VPR;
+    const uint32_t w[4] = {r.sd.x, r.sd.y, r.sd.z, r.sd.w};
+    if (sizeof(TIn) == 2) {
 #pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    const uint32_t w0 = r.kr[0][d], w1 = r.kr[1][d], w2 = r.kr[2][d], w3 = r.kr[3][d];
-    const uint2 ev = make_uint2((w0 & 0xffffu) | (w1 << 16), (w2 & 0xffffu) | (w3 << 16));
-    const uint2 od = make_uint2((w0 >> 16) | (w1 & 0xffff0000u), (w2 >> 16) | (w3 & 0xffff0000u));
-    const int c0 = 8 * cg + 2 * d;
-    *reinterpret_cast<uint2 *>(&Kt[kt_index<F::CP>(c0, p >> 3) + (p & 7)]) = ev;
-    *reinterpret_cast<uint2 *>(&Kt[kt_index<F::CP>(c0 + 1, p >> 3) + (p & 7)]) = od;
+      for (int e = 0; e < 8; ++e)
+        reinterpret_cast<uint16_t *>(&Vl[8 * part + e][tok])[0] =
+            (uint16_t)((w[e >> 1] >> (16 * (e & 1))) & 0xffffu);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) reinterpret_cast<uint32_t *>(&Vl[4 * part + e][tok])[0] = w[e];
+    }
+  } else if (p < CC::SP) {
+    *reinterpret_cast<uint4 *>(&Dl[4 * (p - CC::VP)]) = r.sd;
   }
 }
 
@@ -452,20 +491,46 @@ __device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) 
   return make_uint2(pack_bf16x2(a, b), pack_bf16x2(c, d));
 }
 
-// One chunk of the carry for work-group (pair, value tile): consumes `cur`
-// (fetched one chunk earlier) and prefetches the next chunk into `nxt`.
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// K^T as the A operand of the state update for key tile t, token step s:
+// lane (l16, g4) gets K[j][16 t + l16] for the 8 tokens at positions
+// 32 s + 8 g4 + [0, 8). Each transpose load serves 4 tokens: lanes 4m..4m+3
+// of a 16-lane group point at token j_m, key columns 16 t + 4 (l16 % 4) + [0,4).
+template <int D>
+__device__ __forceinline__ uint4 kt_operand(const uint16_t *Kn, int t, int s,
+                                            int l16, int g4) {
+  uint32_t w[4];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int j = 32 * s + 16 * hh + 4 * g4 + (l16 >> 2);
+    const uint16_t *p = Kn + kn_index<D>(j, 16 * t + 4 * (l16 & 3));
+    const v4i16 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_v4i16 *)(const_cast<uint16_t *>(p)));
+    w[2 * hh] = (uint32_t)(uint16_t)x[0] | ((uint32_t)(uint16_t)x[1] << 16);
+    w[2 * hh + 1] = (uint32_t)(uint16_t)x[2] | ((uint32_t)(uint16_t)x[3] << 16);
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// One chunk of the carry: consumes `cur` (fetched one chunk earlier) and
+// prefetches the next chunk into `nxt`.
 template <int D, int C, typename TIn>
 __device__ __forceinline__ void carry_step(
-    CarryLds<D, C> &L, f32x4 (&S)[Cfg<D, C>::KTW], ChunkRegs<D, C> &cur,
-    ChunkRegs<D, C> &nxt, const CarryLane &ln, int lc, int nch, int64_t seq_t0,
+    CarryLds<D, C, TIn> &L, f32x4 &S, ChunkRegs<D, C> &cur, ChunkRegs<D, C> &nxt,
+    const CarryLane<CarryCfg<D, C>::KP> &ln, int lc, int nch, int64_t seq_t0,
     int64_t seq_t1, int64_t c0, const TIn *__restrict__ q,
     const TIn *__restrict__ k, const TIn *__restrict__ v,
-    const float *__restrict__ beta, const float *__restrict__ gam_ws,
-    const uint16_t *__restrict__ tfrag, const uint16_t *__restrict__ pfrag,
-    TIn *__restrict__ o, int h, int hk, int hqk, int hv, int v0, int tid) {
+    const float *__restrict__ dec_ws, const uint16_t *__restrict__ tfrag,
+    const uint16_t *__restrict__ pfrag, TIn *__restrict__ o, int h, int hk,
+    int hqk, int hv, int v0, int tid) {
   using F = Cfg<D, C>;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
-  const int ib = wave;
+  const bool tgroup = wave < 4;           // X / Y / U wavefronts
+  const int ib = wave & 3;                // token block
+  const bool blk = (F::NIB == 4) || (ib < F::NIB);
+  const bool own = (F::NKT == 8) || (wave < F::NKT);   // owns key tile `wave`
   const int b = lc & 1;
   const int64_t t0 = seq_t0 + (int64_t)lc * C;
   const int nvalid = (int)min((int64_t)C, seq_t1 - t0);
@@ -474,94 +539,116 @@ __device__ __forceinline__ void carry_step(
     // iteration issues the same loads).
     const int lnx = min(lc + 1, nch - 1);
     const int64_t t1 = seq_t0 + (int64_t)lnx * C;
-    carry_fetch<D, C, TIn>(nxt, ln, q, k, v, beta, gam_ws, tfrag, pfrag, t1,
+    carry_fetch<D, C, TIn>(nxt, ln, tgroup, q, k, v, dec_ws, tfrag, pfrag, t1,
                            (int)min((int64_t)C, seq_t1 - t1), (c0 + lnx) * hv + h,
                            h, hk, hqk, hv, v0);
   }
-  const float gcur[4] = {cur.gg.x, cur.gg.y, cur.gg.z, cur.gg.w};
+  const int tb = 16 * min(ib, F::NIB - 1) + 4 * g4;  // this lane's first token
+  const float4 ge4 = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
+  const float4 he4 = *reinterpret_cast<const float4 *>(&L.Dl[b][C + tb]);
+  const float ge[4] = {ge4.x, ge4.y, ge4.z, ge4.w};
+  const float he[4] = {he4.x, he4.y, he4.z, he4.w};
+  const float dl = L.Dl[b][C - 1];
   const int ypos = 32 * (ib >> 1) + 8 * g4 + 4 * (ib & 1);  // tok_pos(16 ib + 4 g4)
 
-  // X = K S^T and Q S^T for token block ib; Y = beta (V - exp(gamma) X).
-  f32x4 qs = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (ib < F::NIB) {
-    f32x4 x = qs;
+  // X = K S^T (waves 0-3) or Q S^T (waves 4-7) for token block ib.
+  f32x4 xs = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (blk) {
+    const uint16_t *A = tgroup ? L.Kn[b] : L.Qn;
 #pragma unroll
     for (int s = 0; s < F::DS; ++s) {
       const uint4 bs = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
-      const uint4 ak = *reinterpret_cast<const uint4 *>(&L.Kn[b][kn_index<D>(16 * ib + l16, 4 * s + g4)]);
-      x = mfma_16x16x32(ak, bs, x);
-      qs = mfma_16x16x32(cur.qa[s], bs, qs);
+      const uint4 a = *reinterpret_cast<const uint4 *>(&A[kn_index<D>(16 * ib + l16, 32 * s + 8 * g4)]);
+      xs = mfma_16x16x32(a, bs, xs);
     }
-    float y[4];
+    if (tgroup) {  // Y = V - exp(gamma) X  (beta is folded into T')
+      float vv[4];
+      Elem<TIn>::load4(&L.Vl[b][l16][tb], vv);
+      float y[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) y[e] = cur.bb[e] * (cur.vv[e] - __expf(gcur[e]) * x[e]);
-    *reinterpret_cast<uint2 *>(&L.Yl[l16 * F::LDV + ypos]) = pack4_bf16(y[0], y[1], y[2], y[3]);
+      for (int e = 0; e < 4; ++e) y[e] = vv[e] - ge[e] * xs[e];
+      *reinterpret_cast<uint2 *>(&L.Yl[l16 * F::LDV + ypos]) = pack4_bf16(y[0], y[1], y[2], y[3]);
+    }
   }
   lds_barrier();
 
-  // U = T Y; also the decay-to-chunk-end scaled copy used by the update.
-  if (ib < F::NIB) {
-    f32x4 u = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (tgroup) {
+    // U = T Y, and the decay-to-chunk-end scaled copy used by the update.
+    if (blk) {
+      f32x4 u = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < F::KS; ++s) {
-      const uint4 by = *reinterpret_cast<const uint4 *>(&L.Yl[l16 * F::LDV + 32 * s + 8 * g4]);
-      u = mfma_16x16x32(cur.ta[s], by, u);
+      for (int s = 0; s < F::KS; ++s) {
+        const uint4 by = *reinterpret_cast<const uint4 *>(&L.Yl[l16 * F::LDV + 32 * s + 8 * g4]);
+        u = mfma_16x16x32(cur.fa[s], by, u);
+      }
+      float uh[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) uh[e] = he[e] * u[e];
+      *reinterpret_cast<uint2 *>(&L.Ul[l16 * F::LDV + ypos]) = pack4_bf16(u[0], u[1], u[2], u[3]);
+      *reinterpret_cast<uint2 *>(&L.Uh[l16 * F::LDV + ypos]) = pack4_bf16(uh[0], uh[1], uh[2], uh[3]);
     }
-    float uh[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) uh[e] = __expf(cur.glast - gcur[e]) * u[e];
-    *reinterpret_cast<uint2 *>(&L.Ul[l16 * F::LDV + ypos]) = pack4_bf16(u[0], u[1], u[2], u[3]);
-    *reinterpret_cast<uint2 *>(&L.Uh[l16 * F::LDV + ypos]) = pack4_bf16(uh[0], uh[1], uh[2], uh[3]);
+  } else if (lc + 1 < nch) {
+    carry_commit<D, C>(nxt, L.Qn, tid - 256);   // every Q read of this chunk is done
   }
+  if (lc + 1 < nch) carry_commit_small<D, C, TIn>(nxt, L.Vl[b ^ 1], L.Dl[b ^ 1], tid);
   lds_barrier();
 
-  // O = exp(gamma) Q S^T + P U; rows past the sequence end are dropped by
-  // the buffer extent.
-  if (ib < F::NIB) {
+  // O = exp(gamma) Q S^T + P U (waves 4-7); rows past the sequence end are
+  // dropped by the buffer extent.
+  if (!tgroup && blk) {
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < F::KS; ++s) {
       const uint4 bu = *reinterpret_cast<const uint4 *>(&L.Ul[l16 * F::LDV + 32 * s + 8 * g4]);
-      acc = mfma_16x16x32(cur.pa[s], bu, acc);
+      acc = mfma_16x16x32(cur.fa[s], bu, acc);
     }
-    const rsrc_t ro = make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nvalid * hv * D * sizeof(TIn)));
+    // Stage the 16 x 16 output block in LDS ([token][value]) so that it
+    // leaves as 16-byte stores; rows past the sequence end are dropped by the
+    // buffer extent.
+    TIn *ol = reinterpret_cast<TIn *>(L.Ol[ib]);
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      BufElem<TIn>::store1(ro, (uint32_t)((16 * ib + 4 * g4 + e) * hv * D + l16),
-                           __expf(gcur[e]) * qs[e] + acc[e]);
+    for (int e = 0; e < 4; ++e) Elem<TIn>::store1(&ol[(4 * g4 + e) * 16 + l16], ge[e] * xs[e] + acc[e]);
+    wave_lds_fence();
+    constexpr int PPR = (int)sizeof(TIn);        // 16-byte pieces per token row
+    constexpr int EPP = 16 / (int)sizeof(TIn);   // elements per piece
+    if (lane < 16 * PPR) {
+      const int row = lane / PPR, part = lane % PPR;
+      const uint4 x = *reinterpret_cast<const uint4 *>(&ol[row * 16 + part * EPP]);
+      const rsrc_t ro = make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nvalid * hv * D * sizeof(TIn)));
+      __builtin_amdgcn_raw_buffer_store_b128(
+          (__attribute__((ext_vector_type(4))) unsigned int){x.x, x.y, x.z, x.w}, ro,
+          (uint32_t)(((16 * ib + row) * hv * D + part * EPP) * sizeof(TIn)), 0, 0);
+    }
   }
 
-  // S^T <- exp(gamma_last) S^T + K^T Uh, one 16-key tile at a time.
-  const float dl = __expf(cur.glast);
-#pragma unroll
-  for (int m = 0; m < F::KTW; ++m) {
-    const int t = wave + 4 * m;
-    if (t >= F::NKT) continue;
-    f32x4 acc = S[m] * dl;
+  // S^T <- exp(gamma_last) S^T + K^T Uh for key tile `wave`.
+  if (own) {
+    f32x4 acc = S * dl;
 #pragma unroll
     for (int s = 0; s < F::KS; ++s) {
-      const uint4 ak = *reinterpret_cast<const uint4 *>(&L.Kt[b][kt_index<F::CP>(16 * t + l16, 4 * s + g4)]);
+      const uint4 a = kt_operand<D>(L.Kn[b], wave, s, l16, g4);
       const uint4 bu = *reinterpret_cast<const uint4 *>(&L.Uh[l16 * F::LDV + 32 * s + 8 * g4]);
-      acc = mfma_16x16x32(ak, bu, acc);
+      acc = mfma_16x16x32(a, bu, acc);
     }
-    S[m] = acc;
-    *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * t + 4 * g4]) =
+    S = acc;
+    *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
         pack4_bf16(acc[0], acc[1], acc[2], acc[3]);
   }
-  if (lc + 1 < nch) carry_commit_k<D, C>(nxt, L.Kn[b ^ 1], L.Kt[b ^ 1], tid);
+  if (tgroup && lc + 1 < nch) carry_commit<D, C>(nxt, L.Kn[b ^ 1], tid);
   lds_barrier();
 }
 
 template <int D, int C, typename TIn>
-__global__ __launch_bounds__(256) void chunk_carry_kernel(
+__global__ __launch_bounds__(512) void chunk_carry_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k,
     const TIn *__restrict__ v, const float *__restrict__ beta,
     const int32_t *__restrict__ cu, const int32_t *__restrict__ off,
-    const float *__restrict__ gam_ws, const uint16_t *__restrict__ tfrag,
+    const float *__restrict__ dec_ws, const uint16_t *__restrict__ tfrag,
     const uint16_t *__restrict__ pfrag, const float *s0, float *sT,
     TIn *__restrict__ o, int hqk, int hv, int group, int n_pairs) {
   using F = Cfg<D, C>;
-  __shared__ __attribute__((aligned(16))) CarryLds<D, C> L;
+  using CC = CarryCfg<D, C>;
+  __shared__ __attribute__((aligned(16))) CarryLds<D, C, TIn> L;
 
   // Work-groups are dealt to the 8 XCDs round-robin by id. Give each XCD
   // whole (sequence, head) pairs with their value tiles adjacent, so the
@@ -579,78 +666,74 @@ __global__ __launch_bounds__(256) void chunk_carry_kernel(
   const int64_t seq_t0 = cu[n], seq_t1 = cu[n + 1];
   const int nch = off[n + 1] - off[n];
   const int64_t c0 = off[n];
+  const bool own = (F::NKT == 8) || (wave < F::NKT);
 
   // Loop-invariant lane offsets (clamped so idle lanes issue valid loads).
-  CarryLane ln;
+  // Thread tid fetches pieces p = tid % 256 + 256 u of K (waves 0-3) or of Q
+  // (waves 4-7), the numbering carry_commit uses.
+  CarryLane<CC::KP> ln;
   {
-    const int ibc = min(wave, F::NIB - 1);
-    const int piece = min(tid, F::PIECES - 1);
-    const int rg = piece % (C / 4), cg = piece / (C / 4);
-    ln.k = (uint32_t)(4 * rg * hqk * D + 8 * cg);
-    ln.q = (uint32_t)((16 * ibc + l16) * hqk * D + 8 * g4);
-    ln.v = (uint32_t)((16 * ibc + 4 * g4) * hv * D + l16);
-    ln.b = (uint32_t)((16 * ibc + 4 * g4) * hv);
+    using CS = CarryCfg<D, C, TIn>;
+    const int ibc = min(wave & 3, F::NIB - 1);
+#pragma unroll
+    for (int u = 0; u < CC::KP; ++u) {
+      const int p = min((tid & 255) + (CC::NT / 2) * u, CC::NP - 1);
+      ln.kq[u] = (uint32_t)((p / (D / 8)) * hqk * D + 8 * (p % (D / 8)));
+    }
     ln.frag = (uint32_t)((ibc * F::KS * 64 + lane) * 8);
-    ln.gam = (uint32_t)(16 * ibc + 4 * g4);
+    ln.sd_any = tid < CS::SP;
+    ln.sd_v = tid < CS::VP;
+    ln.sd = ln.sd_v ? (uint32_t)(((tid / CS::VPR) * hv * D + (tid % CS::VPR) * (16 / (int)sizeof(TIn))) * sizeof(TIn))
+                    : (uint32_t)(16 * (tid - CS::VP));
   }
 
   if (C < F::CP) {  // zero the token positions past the chunk, once
-    for (int idx = tid; idx < 16 * F::LDV; idx += 256) {
+    for (int idx = tid; idx < 16 * F::LDV; idx += CC::NT) {
       L.Yl[idx] = 0;
       L.Ul[idx] = 0;
       L.Uh[idx] = 0;
     }
-    for (int idx = tid; idx < 2 * D * F::CP; idx += 256) (&L.Kt[0][0])[idx] = 0;
+    for (int idx = C * D + tid; idx < F::CP * D; idx += CC::NT) {
+      L.Kn[0][idx] = 0;
+      L.Kn[1][idx] = 0;
+    }
+    lds_barrier();
   }
 
-  // State tile rows v0..v0+15; this wave owns key tiles wave + 4m. Lane l
-  // holds S[v0 + l%16][16 t + 4 (l/16) + e] (the accumulator layout of the
+  // State rows v0..v0+15, key tile `wave`: lane l holds
+  // S[v0 + l%16][16 wave + 4 (l/16) + e] (the accumulator layout of the
   // S^T update).
-  f32x4 S[F::KTW];
-#pragma unroll
-  for (int m = 0; m < F::KTW; ++m) {
-    S[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int t = wave + 4 * m;
-    if (t < F::NKT && s0 != nullptr) {
-      const float4 x = *reinterpret_cast<const float4 *>(
-          s0 + ((int64_t)pair * D + v0 + l16) * D + 16 * t + 4 * g4);
-      S[m] = f32x4{x.x, x.y, x.z, x.w};
-    }
+  f32x4 S = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (own && s0 != nullptr) {
+    const float4 x = *reinterpret_cast<const float4 *>(
+        s0 + ((int64_t)pair * D + v0 + l16) * D + 16 * wave + 4 * g4);
+    S = f32x4{x.x, x.y, x.z, x.w};
   }
   if (nch > 0) {  // uniform over the work-group
     ChunkRegs<D, C> ra, rb;
-    carry_fetch<D, C, TIn>(ra, ln, q, k, v, beta, gam_ws, tfrag, pfrag, seq_t0,
-                           (int)min((int64_t)C, seq_t1 - seq_t0), c0 * hv + h, h,
-                           hk, hqk, hv, v0);
-    lds_barrier();  // zero fills done before the first K commit
-#pragma unroll
-    for (int m = 0; m < F::KTW; ++m) {
-      const int t = wave + 4 * m;
-      if (t < F::NKT)
-        *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * t + 4 * g4]) =
-            pack4_bf16(S[m][0], S[m][1], S[m][2], S[m][3]);
-    }
-    carry_commit_k<D, C>(ra, L.Kn[0], L.Kt[0], tid);
+    carry_fetch<D, C, TIn>(ra, ln, wave < 4, q, k, v, dec_ws, tfrag, pfrag,
+                           seq_t0, (int)min((int64_t)C, seq_t1 - seq_t0),
+                           c0 * hv + h, h, hk, hqk, hv, v0);
+    if (own)
+      *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
+          pack4_bf16(S[0], S[1], S[2], S[3]);
+    carry_commit<D, C>(ra, wave < 4 ? L.Kn[0] : L.Qn, tid & 255);
+    carry_commit_small<D, C, TIn>(ra, L.Vl[0], L.Dl[0], tid);
     lds_barrier();
 
     for (int lc = 0; lc < nch; lc += 2) {
       carry_step<D, C, TIn>(L, S, ra, rb, ln, lc, nch, seq_t0, seq_t1, c0, q, k,
-                            v, beta, gam_ws, tfrag, pfrag, o, h, hk, hqk, hv, v0,
-                            tid);
+                            v, dec_ws, tfrag, pfrag, o, h, hk, hqk, hv, v0, tid);
       if (lc + 1 < nch)
         carry_step<D, C, TIn>(L, S, rb, ra, ln, lc + 1, nch, seq_t0, seq_t1, c0,
-                              q, k, v, beta, gam_ws, tfrag, pfrag, o, h, hk, hqk,
-                              hv, v0, tid);
+                              q, k, v, dec_ws, tfrag, pfrag, o, h, hk, hqk, hv,
+                              v0, tid);
     }
   }
 
-#pragma unroll
-  for (int m = 0; m < F::KTW; ++m) {
-    const int t = wave + 4 * m;
-    if (t < F::NKT)
-      *reinterpret_cast<float4 *>(sT + ((int64_t)pair * D + v0 + l16) * D + 16 * t + 4 * g4) =
-          make_float4(S[m][0], S[m][1], S[m][2], S[m][3]);
-  }
+  if (own)
+    *reinterpret_cast<float4 *>(sT + ((int64_t)pair * D + v0 + l16) * D + 16 * wave + 4 * g4) =
+        make_float4(S[0], S[1], S[2], S[3]);
 }
 
 // ============================================================ host side
@@ -663,8 +746,8 @@ PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hv,
   size_t p = 0;
   w.chunk_off = p;
   p = align256(p + sizeof(int32_t) * (size_t)(n_seqs + 1));
-  w.gamma = p;
-  p = align256(p + sizeof(float) * (size_t)nc * hv * chunk);
+  w.decay = p;
+  p = align256(p + sizeof(float) * (size_t)nc * hv * 2 * chunk);
   w.tfrag = p;
   p = align256(p + sizeof(uint16_t) * (size_t)nc * hv * frag_elems(chunk));
   w.pfrag = p;
@@ -678,7 +761,7 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
   using F = Cfg<D, C>;
   char *base = static_cast<char *>(a.workspace);
   int32_t *off = reinterpret_cast<int32_t *>(base + ws.chunk_off);
-  float *gam = reinterpret_cast<float *>(base + ws.gamma);
+  float *dec = reinterpret_cast<float *>(base + ws.decay);
   uint16_t *tf = reinterpret_cast<uint16_t *>(base + ws.tfrag);
   uint16_t *pf = reinterpret_cast<uint16_t *>(base + ws.pfrag);
   const int group = a.hv / a.hqk;
@@ -693,16 +776,16 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
     hipLaunchKernelGGL((chunk_local_kernel<D, C, TIn>), dim3((unsigned)nc, (unsigned)a.hqk),
                        dim3(256), 0, a.stream, (const TIn *)a.q, (const TIn *)a.k,
                        a.g, a.beta, a.cu_seqlens, off, a.n_seqs, a.hqk, a.hv,
-                       group, gam, tf, pf);
+                       group, dec, tf, pf);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
 
   const int n_pairs = a.n_seqs * a.hv;
   const int64_t blocks = (int64_t)8 * ((n_pairs + 7) / 8) * F::NVT;
-  hipLaunchKernelGGL((chunk_carry_kernel<D, C, TIn>), dim3((unsigned)blocks), dim3(256),
+  hipLaunchKernelGGL((chunk_carry_kernel<D, C, TIn>), dim3((unsigned)blocks), dim3(512),
                      0, a.stream, (const TIn *)a.q, (const TIn *)a.k,
-                     (const TIn *)a.v, a.beta, a.cu_seqlens, off, gam, tf, pf,
+                     (const TIn *)a.v, a.beta, a.cu_seqlens, off, dec, tf, pf,
                      a.initial_state, a.final_state, (TIn *)a.o, a.hqk, a.hv,
                      group, n_pairs);
   return hipGetLastError();
