@@ -129,7 +129,7 @@ def main():
     roof_pre = {"bound": "mfma", "achieved": round(pre_tflops, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                "kernel": "gdn_prefill (chunk_offsets + chunk_local + chunk_carry)",
+                "kernel": "gdn_prefill (chunk_local + chunk_carry)",
                 "algorithmic_flop_per_launch": flop,
                 "hbm_view_gbs": round(pbytes / pre_avg / 1e9, 1)}
     roof_dec = {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": PEAK_HBM_GBS,

@@ -43,7 +43,7 @@ size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
   if (n_seqs < 0 || n_tokens < 0 || n_tokens > INT32_MAX) return 0;
   if (check_heads(hqk, hv) != GDN_OK) return 0;
   if (!supported_head(dk, dv) || !supported_chunk(chunk)) return 0;
-  return gdn::prefill_workspace_layout(n_seqs, n_tokens, hv, chunk).total;
+  return gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, dk, chunk).total;
 }
 
 gdn_status gdn_prefill(const void *q, const void *k, const void *v,
@@ -63,7 +63,7 @@ gdn_status gdn_prefill(const void *q, const void *k, const void *v,
   if (!cu_seqlens || !final_state) return GDN_ERR_INVALID_ARG;
   if (n_tokens > 0 && (!q || !k || !v || !g || !beta || !o)) return GDN_ERR_INVALID_ARG;
   const gdn::PrefillWorkspace ws =
-      gdn::prefill_workspace_layout(n_seqs, n_tokens, hv, chunk);
+      gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, dk, chunk);
   if (!workspace || workspace_bytes < ws.total ||
       (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
     return GDN_ERR_WORKSPACE;

@@ -36,10 +36,11 @@ struct PrefillArgs {
 
 // Device workspace carved out of the caller's buffer (all offsets 256-aligned).
 struct PrefillWorkspace {
-  size_t chunk_off;   // int32 [N + 1]: first global chunk index of each sequence
   size_t decay;       // f32  [chunks, HV, 2, C]: exp(gamma_i), exp(gamma_last - gamma_i)
   size_t tfrag;       // bf16 [chunks, HV, FRAG]: (I + A)^-1 in operand order
   size_t pfrag;       // bf16 [chunks, HV, FRAG]: decay-masked Q K^T, same order
+  size_t qfrag;       // bf16 [chunks, HQK, C * D]: Q in operand order
+  size_t kcopy;       // bf16 [chunks, HQK, C, D]: K rounded to bf16 (f32 inputs)
   size_t total;
 };
 
@@ -52,8 +53,8 @@ inline int64_t frag_elems(int chunk) {
 inline int64_t chunk_bound(int n_seqs, int64_t n_tokens, int chunk) {
   return (n_tokens + chunk - 1) / chunk + n_seqs;
 }
-PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hv,
-                                          int chunk);
+PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
+                                          int hv, int d, int chunk);
 
 hipError_t launch_decode(const DecodeArgs &a);
 hipError_t launch_prefill(const PrefillArgs &a, const PrefillWorkspace &ws);

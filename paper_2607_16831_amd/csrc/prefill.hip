@@ -16,16 +16,15 @@
 //
 // which reproduces the token-serial recurrence exactly up to rounding.
 //
-// Three kernels on one stream:
-//   chunk_offsets_kernel  first global chunk index of every sequence (a scan
-//                         of ceil(len/C) on the device; no host read).
+// Two kernels on one stream:
 //   chunk_local_kernel    chunk-parallel: gamma, K K^T and Q K^T on bf16 MFMA,
 //                         A, the triangular inverse in LDS (fp32), P; T and P
 //                         are stored as bf16 in MFMA operand order.
 //   chunk_carry_kernel    one work-group per (sequence, value head, 16-row
 //                         value tile): walks the chunks of its sequence, keeps
 //                         its fp32 state tile in MFMA accumulators and does
-//                         every product on bf16 MFMA with fp32 accumulation.
+//                         every product on bf16 MFMA with fp32 accumulation;
+//                         dedicated wavefronts stream the next chunks into LDS.
 //
 // Every exponent is a non-positive difference (for g <= 0), masked before
 // exp, so strongly decaying inputs cannot overflow.
@@ -34,36 +33,13 @@
 
 namespace gdn {
 
-// ============================================================ chunk offsets
-__global__ __launch_bounds__(256) void chunk_offsets_kernel(
-    const int32_t *__restrict__ cu, int32_t *__restrict__ off, int n_seqs,
-    int chunk) {
-  __shared__ int32_t wave_sum[4];
-  __shared__ int32_t carry;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid == 0) {
-    off[0] = 0;
-    carry = 0;
-  }
-  __syncthreads();
-  for (int base = 0; base < n_seqs; base += 256) {
-    const int n = base + tid;
-    int x = 0;
-    if (n < n_seqs) x = (cu[n + 1] - cu[n] + chunk - 1) / chunk;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const int y = __shfl_up(x, d, 64);
-      if (lane >= d) x += y;
-    }
-    if (lane == 63) wave_sum[wave] = x;
-    __syncthreads();
-    int prefix = carry;
-    for (int w = 0; w < wave; ++w) prefix += wave_sum[w];
-    if (n < n_seqs) off[n + 1] = prefix + x;
-    __syncthreads();
-    if (tid == 255) carry = prefix + x;
-    __syncthreads();
-  }
+// ============================================================ chunk numbering
+// Chunks get global slots without a scan: sequence n owns the slots
+// cu[n] / C + n + [0, ceil(len_n / C)). Consecutive ranges never overlap
+// (cu[n+1] / C + n + 1 >= cu[n] / C + n + ceil(len_n / C)) and every slot is
+// below ceil(T / C) + N, so per-chunk tables sized by that bound suffice.
+__device__ __forceinline__ int64_t first_slot(const int32_t *cu, int n, int chunk) {
+  return (int64_t)cu[n] / chunk + n;
 }
 
 template <int D, int C>
@@ -122,28 +98,33 @@ template <int D, int C, typename TIn>
 __global__ __launch_bounds__(256) void chunk_local_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k,
     const float *__restrict__ g, const float *__restrict__ beta,
-    const int32_t *__restrict__ cu, const int32_t *__restrict__ off,
-    int n_seqs, int hqk, int hv, int group, float *__restrict__ dec_ws,
-    uint16_t *__restrict__ tfrag, uint16_t *__restrict__ pfrag) {
+    const int32_t *__restrict__ cu, int n_seqs, int hqk, int hv, int group,
+    float *__restrict__ dec_ws, uint16_t *__restrict__ tfrag,
+    uint16_t *__restrict__ pfrag, uint16_t *__restrict__ qfrag,
+    uint16_t *__restrict__ kcopy) {
   using F = Cfg<D, C>;
   constexpr int NIB = F::NIB, KS = F::KS;
   constexpr int NP = C * (D / 8);  // 16-byte row pieces of K (and of Q)
   constexpr int NL = (NP + 255) / 256;
   __shared__ __attribute__((aligned(16))) LocalLds<D, C> L;
+  __shared__ int owner;
 
   const int cidx = blockIdx.x;
   const int hk = blockIdx.y;
-  if (cidx >= off[n_seqs]) return;
-  int lo = 0, hi = n_seqs;  // off[lo] <= cidx < off[hi]
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (off[mid] <= cidx) lo = mid; else hi = mid;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // The sequence owning slot cidx, if any (every sequence is tested once).
+  if (tid == 0) owner = -1;
+  __syncthreads();
+  for (int m = tid; m < n_seqs; m += 256) {
+    const int64_t base = first_slot(cu, m, C);
+    if (cidx >= base && cidx < base + (cu[m + 1] - cu[m] + C - 1) / C) owner = m;
   }
-  const int n = lo;
-  const int64_t t0 = cu[n] + (int64_t)(cidx - off[n]) * C;
+  __syncthreads();
+  const int n = owner;
+  if (n < 0) return;
+  const int64_t t0 = cu[n] + (cidx - first_slot(cu, n, C)) * C;
   const int nvalid = (int)min((int64_t)C, (int64_t)cu[n + 1] - t0);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g4 = lane >> 4;
   const int ib = wave;
 
@@ -174,6 +155,25 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     }
   }
   lds_barrier();
+
+  // ---- Q of this chunk for the carry, in the A-operand order of Q S^T:
+  // block ib, step s, lane (l16, g4) holds Q[16 ib + l16][32 s + 8 g4 + (0..7)].
+  // For f32 inputs also a bf16 copy of K, row-major [C][D], for the carry.
+  if (ib < NIB) {
+    const int64_t base = ((int64_t)cidx * hqk + hk) * (C * D);
+    uint16_t *qf = qfrag + base + ((int64_t)ib * F::DS * 64 + lane) * 8;
+#pragma unroll
+    for (int s = 0; s < F::DS; ++s)
+      *reinterpret_cast<uint4 *>(qf + s * 512) =
+          *reinterpret_cast<const uint4 *>(&L.u.kq.Q[(16 * ib + l16) * F::LDK + 32 * s + 8 * g4]);
+    if (sizeof(TIn) == 4) {
+      uint16_t *kc = kcopy + base + (int64_t)(16 * ib + l16) * D;
+#pragma unroll
+      for (int s = 0; s < F::DS; ++s)
+        *reinterpret_cast<uint4 *>(kc + 32 * s + 8 * g4) =
+            *reinterpret_cast<const uint4 *>(&L.u.kq.K[(16 * ib + l16) * F::LDK + 32 * s + 8 * g4]);
+    }
+  }
 
   // ---- Gram tiles for column block ib, row blocks jb <= ib. Lane (l16, g4)
   // element e holds  k_j . k_i  and  k_j . q_i,  j = 16 jb + 4 g4 + e,
@@ -356,135 +356,68 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
 }
 
 // ============================================================ chunk carry
-// One work-group of 8 wavefronts per (sequence, value head, 16-row value
-// tile), two wavefronts per SIMD. Wavefronts 0-3 own token block w of the
-// chunk for X = K S^T, Y and U = T Y; wavefronts 4-7 own token block w - 4 for
-// Q S^T and O; all eight update one 16-key tile of the state each. The next
-// chunk is prefetched into registers while the current one is computed; K and
-// Q go through row-major LDS tiles (16-byte chunks XOR-swizzled by row) and
-// K^T is read from the same tile with the LDS transpose load.
+// One work-group per (sequence, value head, 16-row value tile): ten
+// wavefronts, eight that compute and two that only move data.
 //
-// All global reads go through buffer resources rebuilt per chunk from
-// scalars, so per-lane offsets are loop invariant and rows past the end of
-// the sequence read as zero (beta is zero there, so they contribute exact
-// zeros); stores past the end are dropped by the resource extent.
-template <int D, int C, typename TIn = __bf16>
+// Compute wavefronts 0-3 own token block w of the chunk for X = K S^T, Y and
+// U = T' Y; wavefronts 4-7 own token block w - 4 for Q S^T and O; all eight
+// update one 16-key tile of the state each. The operands only one wavefront
+// needs (its rows of T', P and Q, stored by the chunk-local kernel in operand
+// order) are loaded straight into its registers one chunk ahead, 1 KB per
+// contiguous load. What several wavefronts share goes through LDS: K (rows
+// for X, columns for the state update), the V tile and the decay factors,
+// copied by the two loader wavefronts with buffer-to-LDS loads into the
+// buffer the compute wavefronts are not reading. The loaders also write back
+// the output tiles, which the compute wavefronts stage in LDS.
+//
+// Global reads go through buffer resources: rows past the end of the
+// sequence read as zero (beta is zero there, so they add exact zeros) and
+// stores past the end are dropped by the resource extent.
+template <int D, int C, typename TIn>
 struct CarryCfg {
   using F = Cfg<D, C>;
-  static constexpr int NT = 512;                      // threads
-  static constexpr int NP = C * (D / 8);              // 16-byte pieces of K (or Q)
-  // Wavefronts 0-3 fetch K, wavefronts 4-7 fetch Q: KP pieces per thread.
-  static constexpr int KP = (NP + NT / 2 - 1) / (NT / 2);
-  // Per-chunk small data, fetched by the first threads: the 16-value V tile
-  // of every token (VPR 16-byte pieces per token) and the 2C decay factors.
-  static constexpr int VPR = (16 * (int)sizeof(TIn)) / 16;
-  static constexpr int VP = C * VPR;
-  static constexpr int SP = VP + (2 * C) / 4;
-  static_assert(SP <= NT, "small data fits one piece per thread");
+  static constexpr int NCW = 8;                  // compute wavefronts
+  static constexpr int NLW = 2;                  // loader wavefronts
+  static constexpr int NT = 64 * (NCW + NLW);    // threads
+  static constexpr int ESZ = (int)sizeof(TIn);
+  static constexpr int KPR = D / 8;              // 16-byte units per bf16 K row
+  static constexpr int NKI = C * D / 512;        // 1 KB copies per K chunk
+  static constexpr int VPR = ESZ;                // 16-byte units per token of a V/O tile row
+  static constexpr int VU = C * VPR;             // 16-byte units of the V (or O) tile
+  static constexpr int NVI = (VU + 63) / 64;     // 1 KB copies per V tile
+  static constexpr int NDI = (2 * C + 63) / 64;  // 256-byte copies of the 2C decay factors
+  static constexpr int M = NKI + NVI + NDI;      // copies per chunk
+  static constexpr int SLOTS = (M + NLW - 1) / NLW;
+  static constexpr int NOU = (VU + 64 * NLW - 1) / (64 * NLW);  // output units per loader lane
+  static_assert(NT == 640, "launch bounds of the carry kernel");
 };
 
-template <int D, int C>
-struct ChunkRegs {
-  using F = Cfg<D, C>;
-  uint4 kq[CarryCfg<D, C>::KP];   // K pieces (waves 0-3) or Q pieces (4-7)
-  uint4 fa[F::KS];   // T' fragments (waves 0-3) or P fragments (waves 4-7)
-  uint4 sd;          // one piece of the V tile or of the decay factors
-};
-
-// Per-lane offsets, fixed for the whole sequence.
-template <int KP>
-struct CarryLane {
-  uint32_t kq[KP];   // elements
-  uint32_t frag;     // elements
-  uint32_t sd;       // bytes, into V (sd_v) or the decay row
-  bool sd_v, sd_any;
-};
-
-template <int D, int C, typename TIn>
-__device__ __forceinline__ void carry_fetch(
-    ChunkRegs<D, C> &r, const CarryLane<CarryCfg<D, C>::KP> &ln, bool tgroup,
-    const TIn *__restrict__ q, const TIn *__restrict__ k,
-    const TIn *__restrict__ v, const float *__restrict__ dec_ws,
-    const uint16_t *__restrict__ tfrag, const uint16_t *__restrict__ pfrag,
-    int64_t t0, int nvalid, int64_t slot, int h, int hk, int hqk, int hv,
-    int v0) {
-  using F = Cfg<D, C>;
-  const rsrc_t rkq = make_rsrc((tgroup ? k : q) + (t0 * hqk + hk) * D,
-                               (uint32_t)(nvalid * hqk * D * sizeof(TIn)));
-  const rsrc_t rf = make_rsrc((tgroup ? tfrag : pfrag) + slot * F::FRAG, F::FRAG * 2);
-#pragma unroll
-  for (int u = 0; u < CarryCfg<D, C>::KP; ++u) r.kq[u] = BufElem<TIn>::load8(rkq, ln.kq[u]);
-#pragma unroll
-  for (int s = 0; s < F::KS; ++s) r.fa[s] = buf_load_b128(rf, (ln.frag + s * 512) * 2);
-  if (ln.sd_any) {
-    const rsrc_t rs = ln.sd_v
-        ? make_rsrc(v + (t0 * hv + h) * D + v0, (uint32_t)(nvalid * hv * D * sizeof(TIn)))
-        : make_rsrc(dec_ws + slot * 2 * C, 2 * C * 4);
-    r.sd = buf_load_b128(rs, ln.sd);
-  }
-}
+constexpr int kCarryThreads = 640;
 
 template <int D, int C, typename TIn>
 struct CarryLds {
   using F = Cfg<D, C>;
-  uint16_t Kn[2][F::CP * D];    // K chunk, row-major, swizzled (double buffered);
-                                // rows C..CP-1 stay zero for chunks below 32
-  uint16_t Qn[C * D];           // Q chunk, same layout (read before the first
-                                // barrier of a chunk, refilled after it)
-  TIn Vl[2][16][C + 8];         // V tile, [value][token], input element type
-  float Dl[2][2 * C];           // exp(gamma_i), then exp(gamma_last - gamma_i)
+  using CC = CarryCfg<D, C, TIn>;
+  uint16_t Kn[2][F::CP * D];    // K chunk, row-major, swizzled; rows C..CP-1 stay zero
+  uint4 Vl[2][CC::NVI * 64];    // V tile, [token][16 values], input element type
+  uint4 Ol[2][CC::NVI * 64];    // output tile, same layout
+  float Dl[2][CC::NDI * 64];    // exp(gamma_i), then exp(gamma_last - gamma_i)
   uint16_t Sl[16 * F::LDK];     // bf16 copy of the state tile, [value][key]
   uint16_t Yl[16 * F::LDV];     // Y,  [value][token position]
   uint16_t Ul[16 * F::LDV];     // U,  [value][token position]
   uint16_t Uh[16 * F::LDV];     // exp(gamma_last - gamma) U, same layout
-  uint32_t Ol[4][16 * 16 * 4 / 4];  // per-wavefront output staging (fp32 worst case)
 };
 
-// Element index of (row, column) in a swizzled row-major [C][D] tile: 16-byte
-// chunks are XORed with a row function so that both 16 consecutive rows at
-// one column (matrix-operand reads) and 16 chunks of one row (the commit)
-// fall on distinct bank groups.
+// Element index of (row, column) in a swizzled row-major [rows][D] tile:
+// 16-byte chunks are XORed with a row function so that 16 consecutive rows
+// at one column (matrix-operand reads) fall on distinct bank groups.
+template <int D>
+__device__ __forceinline__ int kn_swizzle(int row) {
+  return ((row & 15) ^ ((row >> 4) & 3)) & (D / 8 - 1);
+}
 template <int D>
 __device__ __forceinline__ int kn_index(int row, int col) {
-  const int sw = ((row & 15) ^ ((row >> 4) & 3)) & (D / 8 - 1);
-  return row * D + 8 * ((col >> 3) ^ sw) + (col & 7);
-}
-
-// Pieces p = tid4 + 256 u of K (waves 0-3) or Q (waves 4-7), tid4 = tid % 256.
-template <int D, int C>
-__device__ __forceinline__ void carry_commit(const ChunkRegs<D, C> &r,
-                                             uint16_t *dst, int tid4) {
-  using CC = CarryCfg<D, C>;
-#pragma unroll
-  for (int u = 0; u < CC::KP; ++u) {
-    const int p = tid4 + (CC::NT / 2) * u;
-    if (CC::NP % (CC::NT / 2) != 0 && p >= CC::NP) continue;
-    *reinterpret_cast<uint4 *>(&dst[kn_index<D>(p / (D / 8), 8 * (p % (D / 8)))]) = r.kq[u];
-  }
-}
-
-// Small-data piece p of the thread: V pieces go to the [value][token] tile,
-// decay quads to their row.
-template <int D, int C, typename TIn>
-__device__ __forceinline__ void carry_commit_small(const ChunkRegs<D, C> &r,
-                                                   TIn (*Vl)[C + 8], float *Dl,
-                                                   int p) {
-  using CC = CarryCfg<D, C, TIn>;
-  if (p < CC::VP) {
-    const int tok = p / CC::VPR, part = p % CC::VPR;
-    const uint32_t w[4] = {r.sd.x, r.sd.y, r.sd.z, r.sd.w};
-    if (sizeof(TIn) == 2) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        reinterpret_cast<uint16_t *>(&Vl[8 * part + e][tok])[0] =
-            (uint16_t)((w[e >> 1] >> (16 * (e & 1))) & 0xffffu);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) reinterpret_cast<uint32_t *>(&Vl[4 * part + e][tok])[0] = w[e];
-    }
-  } else if (p < CC::SP) {
-    *reinterpret_cast<uint4 *>(&Dl[4 * (p - CC::VP)]) = r.sd;
-  }
+  return row * D + 8 * ((col >> 3) ^ kn_swizzle<D>(row)) + (col & 7);
 }
 
 __device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) {
@@ -493,6 +426,7 @@ __device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) 
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) void lds_void;
 
 // K^T as the A operand of the state update for key tile t, token step s:
 // lane (l16, g4) gets K[j][16 t + l16] for the 8 tokens at positions
@@ -514,140 +448,335 @@ __device__ __forceinline__ uint4 kt_operand(const uint16_t *Kn, int t, int s,
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// One chunk of the carry: consumes `cur` (fetched one chunk earlier) and
-// prefetches the next chunk into `nxt`.
+constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond every resource: reads 0
+
+// ---------------------------------------------------------------- loaders
+// Copy m of a chunk, in order: K (1 KB each), V tile (1 KB each), decay
+// factors (256 bytes each). A buffer-to-LDS load writes lane i's bytes at
+// LDS base + i * size, so the per-lane source offset chooses what lands
+// where: for K it undoes the row swizzle. The offsets do not change from
+// chunk to chunk.
 template <int D, int C, typename TIn>
-__device__ __forceinline__ void carry_step(
-    CarryLds<D, C, TIn> &L, f32x4 &S, ChunkRegs<D, C> &cur, ChunkRegs<D, C> &nxt,
-    const CarryLane<CarryCfg<D, C>::KP> &ln, int lc, int nch, int64_t seq_t0,
-    int64_t seq_t1, int64_t c0, const TIn *__restrict__ q,
-    const TIn *__restrict__ k, const TIn *__restrict__ v,
-    const float *__restrict__ dec_ws, const uint16_t *__restrict__ tfrag,
-    const uint16_t *__restrict__ pfrag, TIn *__restrict__ o, int h, int hk,
-    int hqk, int hv, int v0, int tid) {
-  using F = Cfg<D, C>;
-  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
-  const bool tgroup = wave < 4;           // X / Y / U wavefronts
-  const int ib = wave & 3;                // token block
-  const bool blk = (F::NIB == 4) || (ib < F::NIB);
-  const bool own = (F::NKT == 8) || (wave < F::NKT);   // owns key tile `wave`
-  const int b = lc & 1;
-  const int64_t t0 = seq_t0 + (int64_t)lc * C;
-  const int nvalid = (int)min((int64_t)C, seq_t1 - t0);
-  {
-    // Prefetch the next chunk (the last chunk re-reads itself, so every
-    // iteration issues the same loads).
-    const int lnx = min(lc + 1, nch - 1);
-    const int64_t t1 = seq_t0 + (int64_t)lnx * C;
-    carry_fetch<D, C, TIn>(nxt, ln, tgroup, q, k, v, dec_ws, tfrag, pfrag, t1,
-                           (int)min((int64_t)C, seq_t1 - t1), (c0 + lnx) * hv + h,
-                           h, hk, hqk, hv, v0);
+__device__ __forceinline__ uint32_t copy_offset(int m, int lane, int kstride, int hv) {
+  using CC = CarryCfg<D, C, TIn>;
+  if (m < CC::NKI) {
+    const int u = 64 * m + lane, row = u / CC::KPR;
+    const int jl = (u % CC::KPR) ^ kn_swizzle<D>(row);
+    return (uint32_t)((row * kstride + 8 * jl) * 2);
+  } else if (m < CC::NKI + CC::NVI) {
+    const int u = 64 * (m - CC::NKI) + lane;
+    if (u >= CC::VU) return kOutOfRange;
+    return (uint32_t)(((u / CC::VPR) * hv * D + (u % CC::VPR) * (16 / CC::ESZ)) * CC::ESZ);
+  } else if (m < CC::M) {
+    const int u = 64 * (m - CC::NKI - CC::NVI) + lane;
+    return u < 2 * C ? (uint32_t)(4 * u) : kOutOfRange;
   }
-  const int tb = 16 * min(ib, F::NIB - 1) + 4 * g4;  // this lane's first token
-  const float4 ge4 = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
-  const float4 he4 = *reinterpret_cast<const float4 *>(&L.Dl[b][C + tb]);
-  const float ge[4] = {ge4.x, ge4.y, ge4.z, ge4.w};
-  const float he[4] = {he4.x, he4.y, he4.z, he4.w};
-  const float dl = L.Dl[b][C - 1];
-  const int ypos = 32 * (ib >> 1) + 8 * g4 + 4 * (ib & 1);  // tok_pos(16 ib + 4 g4)
+  return kOutOfRange;
+}
 
-  // X = K S^T (waves 0-3) or Q S^T (waves 4-7) for token block ib.
-  f32x4 xs = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (blk) {
-    const uint16_t *A = tgroup ? L.Kn[b] : L.Qn;
-#pragma unroll
-    for (int s = 0; s < F::DS; ++s) {
-      const uint4 bs = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
-      const uint4 a = *reinterpret_cast<const uint4 *>(&A[kn_index<D>(16 * ib + l16, 32 * s + 8 * g4)]);
-      xs = mfma_16x16x32(a, bs, xs);
-    }
-    if (tgroup) {  // Y = V - exp(gamma) X  (beta is folded into T')
-      float vv[4];
-      Elem<TIn>::load4(&L.Vl[b][l16][tb], vv);
-      float y[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) y[e] = vv[e] - ge[e] * xs[e];
-      *reinterpret_cast<uint2 *>(&L.Yl[l16 * F::LDV + ypos]) = pack4_bf16(y[0], y[1], y[2], y[3]);
-    }
+struct CopyRes {
+  rsrc_t k, v, d;
+};
+
+template <int D, int C, typename TIn>
+__device__ __forceinline__ void issue_copy(CarryLds<D, C, TIn> &L, int bb, const CopyRes &R,
+                                           int m, uint32_t off) {
+  using CC = CarryCfg<D, C, TIn>;
+  if (m < CC::NKI) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(R.k, (lds_void *)&L.Kn[bb][512 * m], 16, off, 0, 0, 0);
+  } else if (m < CC::NKI + CC::NVI) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(R.v, (lds_void *)&L.Vl[bb][64 * (m - CC::NKI)], 16, off, 0, 0, 0);
+  } else if (m < CC::M) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(R.d, (lds_void *)&L.Dl[bb][64 * (m - CC::NKI - CC::NVI)], 4, off, 0, 0, 0);
   }
-  lds_barrier();
+}
 
-  if (tgroup) {
-    // U = T Y, and the decay-to-chunk-end scaled copy used by the update.
-    if (blk) {
-      f32x4 u = f32x4{0.f, 0.f, 0.f, 0.f};
+// Output tile of one chunk, staged in LDS as [token][16 values], to global.
+template <int D, int C, typename TIn>
+__device__ __forceinline__ void store_out(const CarryLds<D, C, TIn> &L, int bb, rsrc_t ro,
+                                          const int *op, const uint32_t *ooff) {
+  using CC = CarryCfg<D, C, TIn>;
 #pragma unroll
-      for (int s = 0; s < F::KS; ++s) {
-        const uint4 by = *reinterpret_cast<const uint4 *>(&L.Yl[l16 * F::LDV + 32 * s + 8 * g4]);
-        u = mfma_16x16x32(cur.fa[s], by, u);
-      }
-      float uh[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) uh[e] = he[e] * u[e];
-      *reinterpret_cast<uint2 *>(&L.Ul[l16 * F::LDV + ypos]) = pack4_bf16(u[0], u[1], u[2], u[3]);
-      *reinterpret_cast<uint2 *>(&L.Uh[l16 * F::LDV + ypos]) = pack4_bf16(uh[0], uh[1], uh[2], uh[3]);
-    }
-  } else if (lc + 1 < nch) {
-    carry_commit<D, C>(nxt, L.Qn, tid - 256);   // every Q read of this chunk is done
-  }
-  if (lc + 1 < nch) carry_commit_small<D, C, TIn>(nxt, L.Vl[b ^ 1], L.Dl[b ^ 1], tid);
-  lds_barrier();
-
-  // O = exp(gamma) Q S^T + P U (waves 4-7); rows past the sequence end are
-  // dropped by the buffer extent.
-  if (!tgroup && blk) {
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < F::KS; ++s) {
-      const uint4 bu = *reinterpret_cast<const uint4 *>(&L.Ul[l16 * F::LDV + 32 * s + 8 * g4]);
-      acc = mfma_16x16x32(cur.fa[s], bu, acc);
-    }
-    // Stage the 16 x 16 output block in LDS ([token][value]) so that it
-    // leaves as 16-byte stores; rows past the sequence end are dropped by the
-    // buffer extent.
-    TIn *ol = reinterpret_cast<TIn *>(L.Ol[ib]);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) Elem<TIn>::store1(&ol[(4 * g4 + e) * 16 + l16], ge[e] * xs[e] + acc[e]);
-    wave_lds_fence();
-    constexpr int PPR = (int)sizeof(TIn);        // 16-byte pieces per token row
-    constexpr int EPP = 16 / (int)sizeof(TIn);   // elements per piece
-    if (lane < 16 * PPR) {
-      const int row = lane / PPR, part = lane % PPR;
-      const uint4 x = *reinterpret_cast<const uint4 *>(&ol[row * 16 + part * EPP]);
-      const rsrc_t ro = make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nvalid * hv * D * sizeof(TIn)));
+  for (int j = 0; j < CC::NOU; ++j) {
+    if (op[j] < CC::VU) {
+      const uint4 x = L.Ol[bb][op[j]];
       __builtin_amdgcn_raw_buffer_store_b128(
-          (__attribute__((ext_vector_type(4))) unsigned int){x.x, x.y, x.z, x.w}, ro,
-          (uint32_t)(((16 * ib + row) * hv * D + part * EPP) * sizeof(TIn)), 0, 0);
+          (__attribute__((ext_vector_type(4))) unsigned int){x.x, x.y, x.z, x.w}, ro, ooff[j], 0, 0);
     }
   }
+}
 
-  // S^T <- exp(gamma_last) S^T + K^T Uh for key tile `wave`.
-  if (own) {
-    f32x4 acc = S * dl;
+// Loader wavefront LW (a template parameter, so that the kind of each of its
+// copies is known when compiling).
+template <int D, int C, typename TIn, int LW>
+__device__ __forceinline__ void carry_loader(
+    CarryLds<D, C, TIn> &L, int lane, const uint16_t *__restrict__ ksrc, int kstride,
+    bool kcopied, const TIn *__restrict__ v, const float *__restrict__ dec_ws,
+    TIn *__restrict__ o, int nch, int64_t seq_t0, int64_t seq_t1, int64_t c0, int h,
+    int hk, int hqk, int hv, int v0) {
+  using CC = CarryCfg<D, C, TIn>;
+  constexpr int NS = CC::SLOTS;
+  uint32_t off[NS];
+#pragma unroll
+  for (int i = 0; i < NS; ++i) off[i] = copy_offset<D, C, TIn>(CC::NLW * i + LW, lane, kstride, hv);
+  int op[CC::NOU];
+  uint32_t ooff[CC::NOU];
+#pragma unroll
+  for (int j = 0; j < CC::NOU; ++j) {
+    op[j] = 64 * (LW + CC::NLW * j) + lane;
+    ooff[j] = (uint32_t)(((op[j] / CC::VPR) * hv * D + (op[j] % CC::VPR) * (16 / CC::ESZ)) * CC::ESZ);
+  }
+
+  auto res = [&](int lc) {
+    const int64_t t0 = seq_t0 + (int64_t)lc * C;
+    const int nv = (int)min((int64_t)C, seq_t1 - t0);
+    CopyRes r;
+    if (kcopied)  // bf16 copy in the workspace, [chunk slot][key head][C][D]
+      r.k = make_rsrc(ksrc + ((c0 + lc) * hqk + hk) * (C * D), C * D * 2);
+    else
+      r.k = make_rsrc(ksrc + (t0 * hqk + hk) * D, (uint32_t)(nv * hqk * D * 2));
+    r.v = make_rsrc(v + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * CC::ESZ));
+    r.d = make_rsrc(dec_ws + ((c0 + lc) * hv + h) * 2 * C, 2 * C * 4);
+    return r;
+  };
+  auto out_res = [&](int lc, bool live) {
+    const int64_t t0 = seq_t0 + (int64_t)lc * C;
+    const int nv = live ? (int)min((int64_t)C, seq_t1 - t0) : 0;
+    return make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * CC::ESZ));
+  };
+
+  {  // chunk 0 into buffer 0
+    const CopyRes R = res(0);
+#pragma unroll
+    for (int i = 0; i < NS; ++i) issue_copy<D, C, TIn>(L, 0, R, CC::NLW * i + LW, off[i]);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+  lds_barrier();
+
+  for (int lc = 0; lc < nch; ++lc) {
+    // output of chunk lc - 2 (staged during phase 1 of chunk lc - 1), then
+    // chunk lc + 1 into the buffer chunk lc - 1 used
+    store_out<D, C, TIn>(L, lc & 1, out_res(max(lc - 2, 0), lc >= 2), op, ooff);
+    if (lc + 1 < nch) {
+      const CopyRes R = res(lc + 1);
+#pragma unroll
+      for (int i = 0; i < NS; ++i) issue_copy<D, C, TIn>(L, (lc & 1) ^ 1, R, CC::NLW * i + LW, off[i]);
+    }
+    lds_barrier();
+    lds_barrier();
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    lds_barrier();
+  }
+  // outputs of the last two chunks
+  store_out<D, C, TIn>(L, nch & 1, out_res(max(nch - 2, 0), nch >= 2), op, ooff);
+  lds_barrier();
+  store_out<D, C, TIn>(L, (nch - 1) & 1, out_res(nch - 1, true), op, ooff);
+}
+
+// ---------------------------------------------------------------- compute
+// Per chunk c, three phases separated by work-group barriers:
+//   1. waves 0-3: X = K S^T for their token block, Y = V - exp(gamma) X.
+//      waves 4-7: O of chunk c-1 = exp(gamma) Q S^T + P U (their operands
+//      were kept from chunk c-1; U of chunk c-1 is still in LDS).
+//   2. waves 0-3: U = T' Y and exp(gamma_last - gamma) U.
+//      waves 4-7: Q S^T (S is still the state entering chunk c).
+//   3. all eight: S^T <- exp(gamma_last) S^T + K^T (exp(gamma_last - gamma) U)
+//      for their key tile.
+// The chain from one state to the next runs through phases 1-3 on waves 0-3
+// and the update; the output work fills the phases where it would idle.
+template <int D, int C, typename TIn>
+struct StateTile {
+  uint4 kt[Cfg<D, C>::KS];
+  __device__ __forceinline__ void fetch(const CarryLds<D, C, TIn> &L, int b, int wave, int l16,
+                                        int g4) {
+#pragma unroll
+    for (int s = 0; s < Cfg<D, C>::KS; ++s) kt[s] = kt_operand<D>(L.Kn[b], wave, s, l16, g4);
+  }
+  __device__ __forceinline__ void update(CarryLds<D, C, TIn> &L, f32x4 &S, int b, int wave,
+                                         int l16, int g4) {
+    using F = Cfg<D, C>;
+    f32x4 acc = S * L.Dl[b][C - 1];
 #pragma unroll
     for (int s = 0; s < F::KS; ++s) {
-      const uint4 a = kt_operand<D>(L.Kn[b], wave, s, l16, g4);
       const uint4 bu = *reinterpret_cast<const uint4 *>(&L.Uh[l16 * F::LDV + 32 * s + 8 * g4]);
-      acc = mfma_16x16x32(a, bu, acc);
+      acc = mfma_16x16x32(kt[s], bu, acc);
     }
     S = acc;
     *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
         pack4_bf16(acc[0], acc[1], acc[2], acc[3]);
   }
-  if (tgroup && lc + 1 < nch) carry_commit<D, C>(nxt, L.Kn[b ^ 1], tid);
+};
+
+// Wavefronts 0-3: X, Y and U for token block ib. Each role runs its own loop
+// (with the same barriers) so that every register prefetched for the next
+// chunk is consumed and then reloaded in place.
+template <int D, int C, typename TIn>
+__device__ __forceinline__ void carry_compute_xu(
+    CarryLds<D, C, TIn> &L, f32x4 &S, int wave, int lane, int nch, int64_t c0,
+    const uint16_t *__restrict__ tfrag, int h, int hv) {
+  using F = Cfg<D, C>;
+  const int l16 = lane & 15, g4 = lane >> 4;
+  const int ib = wave;
+  const bool blk = (F::NIB == 4) || (ib < F::NIB);
+  const bool own = (F::NKT == 8) || (wave < F::NKT);
+  const int ibc = min(ib, F::NIB - 1);
+  const int tb = 16 * ibc + 4 * g4;                     // this lane's first token
+  const int ypos = 32 * (ib >> 1) + 8 * g4 + 4 * (ib & 1);  // tok_pos(16 ib + 4 g4)
+  const uint32_t foff = (uint32_t)(((ibc * F::KS) * 64 + lane) * 16);
+  auto frag_res = [&](int lc) {
+    return make_rsrc(tfrag + ((c0 + lc) * hv + h) * F::FRAG, F::FRAG * 2);
+  };
+  uint4 fa[F::KS];   // T' rows of block ib, one chunk ahead
+  {
+    const rsrc_t rt = frag_res(0);
+#pragma unroll
+    for (int s = 0; s < F::KS; ++s) fa[s] = buf_load_b128(rt, foff + 1024u * s);
+  }
+  StateTile<D, C, TIn> st;
+  for (int lc = 0; lc < nch; ++lc) {
+    const int b = lc & 1;
+    // ---- phase 1: X = K S^T, Y = V - exp(gamma) X (beta is folded into T')
+    float he[4];
+    if (blk) {
+      const float4 ge4 = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
+      const float4 he4 = *reinterpret_cast<const float4 *>(&L.Dl[b][C + tb]);
+      he[0] = he4.x; he[1] = he4.y; he[2] = he4.z; he[3] = he4.w;
+      f32x4 xs = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < F::DS; ++s) {
+        const uint4 bs = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
+        const uint4 a = *reinterpret_cast<const uint4 *>(&L.Kn[b][kn_index<D>(16 * ib + l16, 32 * s + 8 * g4)]);
+        xs = mfma_16x16x32(a, bs, xs);
+      }
+      const TIn *vt = reinterpret_cast<const TIn *>(L.Vl[b]);
+      const float ge[4] = {ge4.x, ge4.y, ge4.z, ge4.w};
+      float y[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) y[e] = Elem<TIn>::load1(&vt[(tb + e) * 16 + l16]) - ge[e] * xs[e];
+      *reinterpret_cast<uint2 *>(&L.Yl[l16 * F::LDV + ypos]) = pack4_bf16(y[0], y[1], y[2], y[3]);
+    }
+    lds_barrier();
+    // ---- phase 2: U = T' Y and exp(gamma_last - gamma) U
+    if (blk) {
+      f32x4 u = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < F::KS; ++s) {
+        const uint4 by = *reinterpret_cast<const uint4 *>(&L.Yl[l16 * F::LDV + 32 * s + 8 * g4]);
+        u = mfma_16x16x32(fa[s], by, u);
+      }
+      *reinterpret_cast<uint2 *>(&L.Ul[l16 * F::LDV + ypos]) = pack4_bf16(u[0], u[1], u[2], u[3]);
+      *reinterpret_cast<uint2 *>(&L.Uh[l16 * F::LDV + ypos]) =
+          pack4_bf16(he[0] * u[0], he[1] * u[1], he[2] * u[2], he[3] * u[3]);
+      // reload after the last reader (the last chunk re-reads itself)
+      __builtin_amdgcn_sched_barrier(0);
+      const rsrc_t rt = frag_res(min(lc + 1, nch - 1));
+#pragma unroll
+      for (int s = 0; s < F::KS; ++s) fa[s] = buf_load_b128(rt, foff + 1024u * s);
+    }
+    if (own) st.fetch(L, b, wave, l16, g4);
+    lds_barrier();
+    // ---- phase 3
+    if (own) st.update(L, S, b, wave, l16, g4);
+    lds_barrier();
+  }
+  lds_barrier();  // the output of the last chunk is staged by waves 4-7
+}
+
+// Wavefronts 4-7: Q S^T in phase 2 and, in phase 1 of the next chunk,
+// O = exp(gamma) Q S^T + P U for token block ib (U of that chunk is still in
+// LDS then). The output tile is staged in LDS for the loader wavefronts.
+template <int D, int C, typename TIn>
+__device__ __forceinline__ void carry_compute_o(
+    CarryLds<D, C, TIn> &L, f32x4 &S, int wave, int lane, int nch, int64_t c0,
+    const uint16_t *__restrict__ pfrag, const uint16_t *__restrict__ qfrag, int h, int hk,
+    int hqk, int hv) {
+  using F = Cfg<D, C>;
+  const int l16 = lane & 15, g4 = lane >> 4;
+  const int ib = wave - 4;
+  const bool blk = (F::NIB == 4) || (ib < F::NIB);
+  const bool own = (F::NKT == 8) || (wave < F::NKT);
+  const int ibc = min(ib, F::NIB - 1);
+  const int tb = 16 * ibc + 4 * g4;
+  const uint32_t foff = (uint32_t)(((ibc * F::KS) * 64 + lane) * 16);
+  const uint32_t qoff = (uint32_t)(((ibc * F::DS) * 64 + lane) * 16);
+  auto p_res = [&](int lc) {
+    return make_rsrc(pfrag + ((c0 + lc) * hv + h) * F::FRAG, F::FRAG * 2);
+  };
+  auto q_res = [&](int lc) {
+    return make_rsrc(qfrag + ((c0 + lc) * hqk + hk) * (C * D), C * D * 2);
+  };
+  auto out = [&](int bb, const uint4 *pa, const f32x4 &qs, const float *gq) {
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < F::KS; ++s) {
+      const uint4 bu = *reinterpret_cast<const uint4 *>(&L.Ul[l16 * F::LDV + 32 * s + 8 * g4]);
+      acc = mfma_16x16x32(pa[s], bu, acc);
+    }
+    TIn *ot = reinterpret_cast<TIn *>(L.Ol[bb]);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) Elem<TIn>::store1(&ot[(tb + e) * 16 + l16], gq[e] * qs[e] + acc[e]);
+  };
+  uint4 qf[F::DS];   // Q rows of block ib, one chunk ahead
+  uint4 pa[F::KS];   // P rows of block ib of the previous chunk
+  f32x4 qs = f32x4{0.f, 0.f, 0.f, 0.f};
+  float gq[4] = {0.f, 0.f, 0.f, 0.f};
+  {
+    const rsrc_t rq = q_res(0);
+#pragma unroll
+    for (int s = 0; s < F::DS; ++s) qf[s] = buf_load_b128(rq, qoff + 1024u * s);
+#pragma unroll
+    for (int s = 0; s < F::KS; ++s) pa[s] = make_uint4(0, 0, 0, 0);
+  }
+  StateTile<D, C, TIn> st;
+  for (int lc = 0; lc < nch; ++lc) {
+    const int b = lc & 1;
+    // ---- phase 1: output of chunk lc - 1 (for lc = 0 a zero tile into a
+    // buffer nothing stores), then P of this chunk
+    if (blk) {
+      out(b ^ 1, pa, qs, gq);
+      __builtin_amdgcn_sched_barrier(0);
+      const rsrc_t rp = p_res(lc);
+#pragma unroll
+      for (int s = 0; s < F::KS; ++s) pa[s] = buf_load_b128(rp, foff + 1024u * s);
+    }
+    lds_barrier();
+    // ---- phase 2: Q S^T (S is still the state entering chunk lc)
+    if (blk) {
+      f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < F::DS; ++s) {
+        const uint4 bs = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
+        x = mfma_16x16x32(qf[s], bs, x);
+      }
+      qs = x;
+      const float4 g4v = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
+      gq[0] = g4v.x; gq[1] = g4v.y; gq[2] = g4v.z; gq[3] = g4v.w;
+      // the product must be complete before the registers of Q are reloaded
+      asm volatile("" ::"v"(x) : "memory");
+      const rsrc_t rq = q_res(min(lc + 1, nch - 1));
+#pragma unroll
+      for (int s = 0; s < F::DS; ++s) qf[s] = buf_load_b128(rq, qoff + 1024u * s);
+    }
+    if (own) st.fetch(L, b, wave, l16, g4);
+    lds_barrier();
+    // ---- phase 3
+    if (own) st.update(L, S, b, wave, l16, g4);
+    lds_barrier();
+  }
+  if (blk) out((nch - 1) & 1, pa, qs, gq);   // output of the last chunk
   lds_barrier();
 }
 
 template <int D, int C, typename TIn>
-__global__ __launch_bounds__(512) void chunk_carry_kernel(
-    const TIn *__restrict__ q, const TIn *__restrict__ k,
-    const TIn *__restrict__ v, const float *__restrict__ beta,
-    const int32_t *__restrict__ cu, const int32_t *__restrict__ off,
-    const float *__restrict__ dec_ws, const uint16_t *__restrict__ tfrag,
-    const uint16_t *__restrict__ pfrag, const float *s0, float *sT,
-    TIn *__restrict__ o, int hqk, int hv, int group, int n_pairs) {
+__global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
+    const TIn *__restrict__ k, const TIn *__restrict__ v,
+    const int32_t *__restrict__ cu, const float *__restrict__ dec_ws,
+    const uint16_t *__restrict__ tfrag, const uint16_t *__restrict__ pfrag,
+    const uint16_t *__restrict__ qfrag, const uint16_t *__restrict__ kcopy,
+    const float *s0, float *sT, TIn *__restrict__ o, int hqk, int hv, int group,
+    int n_pairs) {
   using F = Cfg<D, C>;
-  using CC = CarryCfg<D, C>;
+  using CC = CarryCfg<D, C, TIn>;
   __shared__ __attribute__((aligned(16))) CarryLds<D, C, TIn> L;
 
   // Work-groups are dealt to the 8 XCDs round-robin by id. Give each XCD
@@ -661,44 +790,14 @@ __global__ __launch_bounds__(512) void chunk_carry_kernel(
   const int n = pair / hv, h = pair % hv, hk = h / group;
   const int v0 = 16 * vt;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, g4 = lane >> 4;
   const int64_t seq_t0 = cu[n], seq_t1 = cu[n + 1];
-  const int nch = off[n + 1] - off[n];
-  const int64_t c0 = off[n];
-  const bool own = (F::NKT == 8) || (wave < F::NKT);
-
-  // Loop-invariant lane offsets (clamped so idle lanes issue valid loads).
-  // Thread tid fetches pieces p = tid % 256 + 256 u of K (waves 0-3) or of Q
-  // (waves 4-7), the numbering carry_commit uses.
-  CarryLane<CC::KP> ln;
-  {
-    using CS = CarryCfg<D, C, TIn>;
-    const int ibc = min(wave & 3, F::NIB - 1);
-#pragma unroll
-    for (int u = 0; u < CC::KP; ++u) {
-      const int p = min((tid & 255) + (CC::NT / 2) * u, CC::NP - 1);
-      ln.kq[u] = (uint32_t)((p / (D / 8)) * hqk * D + 8 * (p % (D / 8)));
-    }
-    ln.frag = (uint32_t)((ibc * F::KS * 64 + lane) * 8);
-    ln.sd_any = tid < CS::SP;
-    ln.sd_v = tid < CS::VP;
-    ln.sd = ln.sd_v ? (uint32_t)(((tid / CS::VPR) * hv * D + (tid % CS::VPR) * (16 / (int)sizeof(TIn))) * sizeof(TIn))
-                    : (uint32_t)(16 * (tid - CS::VP));
-  }
-
-  if (C < F::CP) {  // zero the token positions past the chunk, once
-    for (int idx = tid; idx < 16 * F::LDV; idx += CC::NT) {
-      L.Yl[idx] = 0;
-      L.Ul[idx] = 0;
-      L.Uh[idx] = 0;
-    }
-    for (int idx = C * D + tid; idx < F::CP * D; idx += CC::NT) {
-      L.Kn[0][idx] = 0;
-      L.Kn[1][idx] = 0;
-    }
-    lds_barrier();
-  }
+  const int nch = (int)((seq_t1 - seq_t0 + C - 1) / C);
+  const int64_t c0 = first_slot(cu, n, C);
+  const bool compute = wave < CC::NCW;
+  const bool own = compute && ((F::NKT == 8) || (wave < F::NKT));
 
   // State rows v0..v0+15, key tile `wave`: lane l holds
   // S[v0 + l%16][16 wave + 4 (l/16) + e] (the accumulator layout of the
@@ -710,24 +809,38 @@ __global__ __launch_bounds__(512) void chunk_carry_kernel(
     S = f32x4{x.x, x.y, x.z, x.w};
   }
   if (nch > 0) {  // uniform over the work-group
-    ChunkRegs<D, C> ra, rb;
-    carry_fetch<D, C, TIn>(ra, ln, wave < 4, q, k, v, dec_ws, tfrag, pfrag,
-                           seq_t0, (int)min((int64_t)C, seq_t1 - seq_t0),
-                           c0 * hv + h, h, hk, hqk, hv, v0);
-    if (own)
-      *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
-          pack4_bf16(S[0], S[1], S[2], S[3]);
-    carry_commit<D, C>(ra, wave < 4 ? L.Kn[0] : L.Qn, tid & 255);
-    carry_commit_small<D, C, TIn>(ra, L.Vl[0], L.Dl[0], tid);
-    lds_barrier();
-
-    for (int lc = 0; lc < nch; lc += 2) {
-      carry_step<D, C, TIn>(L, S, ra, rb, ln, lc, nch, seq_t0, seq_t1, c0, q, k,
-                            v, dec_ws, tfrag, pfrag, o, h, hk, hqk, hv, v0, tid);
-      if (lc + 1 < nch)
-        carry_step<D, C, TIn>(L, S, rb, ra, ln, lc + 1, nch, seq_t0, seq_t1, c0,
-                              q, k, v, dec_ws, tfrag, pfrag, o, h, hk, hqk, hv,
-                              v0, tid);
+    if (compute) {
+      if (C < F::CP) {  // zero the token positions past the chunk, once
+        for (int idx = tid; idx < 16 * F::LDV; idx += 64 * CC::NCW) {
+          L.Yl[idx] = 0;
+          L.Ul[idx] = 0;
+          L.Uh[idx] = 0;
+        }
+        for (int idx = C * D + tid; idx < F::CP * D; idx += 64 * CC::NCW) {
+          L.Kn[0][idx] = 0;
+          L.Kn[1][idx] = 0;
+        }
+      }
+      if (own)
+        *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
+            pack4_bf16(S[0], S[1], S[2], S[3]);
+      lds_barrier();
+      if (wave < 4)
+        carry_compute_xu<D, C, TIn>(L, S, wave, lane, nch, c0, tfrag, h, hv);
+      else
+        carry_compute_o<D, C, TIn>(L, S, wave, lane, nch, c0, pfrag, qfrag, h, hk, hqk, hv);
+    } else {
+      // bf16 K is copied straight from the input; f32 K from its bf16 copy.
+      const bool kcopied = sizeof(TIn) != 2;
+      const uint16_t *ksrc = kcopied ? kcopy : reinterpret_cast<const uint16_t *>(k);
+      const int kstride = kcopied ? D : hqk * D;
+      static_assert(CC::NLW == 2, "loader dispatch below");
+      if (wave == CC::NCW)
+        carry_loader<D, C, TIn, 0>(L, lane, ksrc, kstride, kcopied, v, dec_ws, o, nch, seq_t0,
+                                   seq_t1, c0, h, hk, hqk, hv, v0);
+      else
+        carry_loader<D, C, TIn, 1>(L, lane, ksrc, kstride, kcopied, v, dec_ws, o, nch, seq_t0,
+                                   seq_t1, c0, h, hk, hqk, hv, v0);
     }
   }
 
@@ -739,19 +852,21 @@ __global__ __launch_bounds__(512) void chunk_carry_kernel(
 // ============================================================ host side
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hv,
-                                          int chunk) {
+PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
+                                          int hv, int d, int chunk) {
   PrefillWorkspace w;
   const int64_t nc = chunk_bound(n_seqs, n_tokens, chunk);
   size_t p = 0;
-  w.chunk_off = p;
-  p = align256(p + sizeof(int32_t) * (size_t)(n_seqs + 1));
   w.decay = p;
   p = align256(p + sizeof(float) * (size_t)nc * hv * 2 * chunk);
   w.tfrag = p;
   p = align256(p + sizeof(uint16_t) * (size_t)nc * hv * frag_elems(chunk));
   w.pfrag = p;
   p = align256(p + sizeof(uint16_t) * (size_t)nc * hv * frag_elems(chunk));
+  w.qfrag = p;
+  p = align256(p + sizeof(uint16_t) * (size_t)nc * hqk * chunk * d);
+  w.kcopy = p;
+  p = align256(p + sizeof(uint16_t) * (size_t)nc * hqk * chunk * d);
   w.total = p;
   return w;
 }
@@ -760,34 +875,29 @@ template <int D, int C, typename TIn>
 static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace &ws) {
   using F = Cfg<D, C>;
   char *base = static_cast<char *>(a.workspace);
-  int32_t *off = reinterpret_cast<int32_t *>(base + ws.chunk_off);
   float *dec = reinterpret_cast<float *>(base + ws.decay);
   uint16_t *tf = reinterpret_cast<uint16_t *>(base + ws.tfrag);
   uint16_t *pf = reinterpret_cast<uint16_t *>(base + ws.pfrag);
+  uint16_t *qf = reinterpret_cast<uint16_t *>(base + ws.qfrag);
+  uint16_t *kc = reinterpret_cast<uint16_t *>(base + ws.kcopy);
   const int group = a.hv / a.hqk;
-
-  hipLaunchKernelGGL(chunk_offsets_kernel, dim3(1), dim3(256), 0, a.stream,
-                     a.cu_seqlens, off, a.n_seqs, C);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
 
   const int64_t nc = chunk_bound(a.n_seqs, a.n_tokens, C);
   if (a.n_tokens > 0) {
     hipLaunchKernelGGL((chunk_local_kernel<D, C, TIn>), dim3((unsigned)nc, (unsigned)a.hqk),
                        dim3(256), 0, a.stream, (const TIn *)a.q, (const TIn *)a.k,
-                       a.g, a.beta, a.cu_seqlens, off, a.n_seqs, a.hqk, a.hv,
-                       group, dec, tf, pf);
-    e = hipGetLastError();
+                       a.g, a.beta, a.cu_seqlens, a.n_seqs, a.hqk, a.hv, group, dec,
+                       tf, pf, qf, kc);
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
 
   const int n_pairs = a.n_seqs * a.hv;
   const int64_t blocks = (int64_t)8 * ((n_pairs + 7) / 8) * F::NVT;
-  hipLaunchKernelGGL((chunk_carry_kernel<D, C, TIn>), dim3((unsigned)blocks), dim3(512),
-                     0, a.stream, (const TIn *)a.q, (const TIn *)a.k,
-                     (const TIn *)a.v, a.beta, a.cu_seqlens, off, dec, tf, pf,
-                     a.initial_state, a.final_state, (TIn *)a.o, a.hqk, a.hv,
-                     group, n_pairs);
+  hipLaunchKernelGGL((chunk_carry_kernel<D, C, TIn>), dim3((unsigned)blocks),
+                     dim3(kCarryThreads), 0, a.stream, (const TIn *)a.k, (const TIn *)a.v,
+                     a.cu_seqlens, dec, tf, pf, qf, kc, a.initial_state, a.final_state,
+                     (TIn *)a.o, a.hqk, a.hv, group, n_pairs);
   return hipGetLastError();
 }
 

@@ -45,7 +45,7 @@ def test_workspace_size():
     assert a > 0 and a % 256 == 0
     assert ws(2, 4096, 16, 32, 128, 128, 64) >= a          # more sequences
     assert ws(1, 8192, 16, 32, 128, 128, 64) > a           # more tokens
-    assert ws(1, 0, 16, 32, 128, 128, 64) > 0              # empty batch still scans
+    assert ws(1, 0, 16, 32, 128, 128, 64) > 0              # one (empty) chunk slot
     assert ws(1, 4096, 16, 32, 128, 128, 48) == 0          # chunk not built
     assert ws(1, 4096, 16, 32, 96, 96, 64) == 0            # head size not built
     assert ws(1, 4096, 16, 24, 128, 128, 64) == 0          # HV % HQK != 0
