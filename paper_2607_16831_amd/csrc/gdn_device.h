@@ -159,6 +159,27 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
+// Lane move of a DPP control (row shift or row broadcast); lanes without a
+// source, and rows outside ROW_MASK, receive 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_or_zero(float x) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROW_MASK, 0xf, false));
+}
+
+// Inclusive prefix sum over the 64 lanes of a wavefront: row shifts by 1, 2,
+// 4 and 8 scan each 16-lane row, then row broadcasts of lanes 15 and 31 carry
+// the running totals into the later rows.
+__device__ __forceinline__ float wave_prefix_sum(float x) {
+  x += dpp_or_zero<0x111, 0xf>(x);  // row_shr:1
+  x += dpp_or_zero<0x112, 0xf>(x);  // row_shr:2
+  x += dpp_or_zero<0x114, 0xf>(x);  // row_shr:4
+  x += dpp_or_zero<0x118, 0xf>(x);  // row_shr:8
+  x += dpp_or_zero<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+  x += dpp_or_zero<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
+
 // ---------------------------------------------------------------- barriers
 // Work-group barrier that orders LDS traffic only. Unlike __syncthreads() it
 // does not wait for outstanding global loads and stores, so prefetches stay

@@ -70,63 +70,121 @@ __device__ __forceinline__ int tok_pos(int j) {
   return (j & ~31) + 8 * ((r >> 2) & 3) + 4 * (r >> 4) + (r & 3);
 }
 
+// ============================================================ swizzled tiles
+// Element index of (row, column) in a swizzled row-major [rows][D] bf16 tile:
+// 16-byte chunks are XORed with a row function so that 16 consecutive rows
+// at one column (matrix-operand reads) fall on distinct bank groups.
+template <int D>
+__device__ __forceinline__ int kn_swizzle(int row) {
+  return ((row & 15) ^ ((row >> 4) & 3)) & (D / 8 - 1);
+}
+template <int D>
+__device__ __forceinline__ int kn_index(int row, int col) {
+  return row * D + 8 * ((col >> 3) ^ kn_swizzle<D>(row)) + (col & 7);
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
 // ============================================================ chunk-local
-// One work-group per (chunk, key head): gamma, K K^T and K Q^T once, then for
-// every value head of the group A, P and T = (I + A)^-1, written as bf16
-// A-operand fragments. T is built from its 16x16 blocks in fp32: wavefront b
-// inverts diagonal block b as (I - M)(I + M^2)(I + M^4)(I + M^8) (M strictly
-// triangular, so the product is exact), then forms its block row from
+// One work-group per (chunk, value head): gamma, K K^T and K Q^T, then A, P
+// and T = (I + A)^-1, written as bf16 A-operand fragments. The two Gram
+// products depend only on the key head; the value heads of a GQA group each
+// recompute them (a few dozen matrix instructions) rather than share a
+// longer work-group, and the launch order puts the heads of one group on
+// the same XCD so that the second reads K and Q from its L2.
+//
+// The 16x16 tiles of the two lower-triangular Gram products are dealt out
+// evenly: wavefront w computes product (w & 1) (0: K K^T for A, 1: K Q^T
+// for P) for the block rows of row set (w >> 1).
+//
+// T is built from its 16x16 blocks in fp32. Diagonal block b is inverted by
+// forward substitution on the vector ALU (one lane per column, all blocks at
+// once in one wavefront); wavefront b then forms its block row from
 //   T[b][c] = -(sum_{m=c+1..b} T[b][m] A[m][c]) T[c][c]^-1    (c < b),
 // carried in transposed form so that every intermediate stays in the
 // accumulator layout of the fp32 16x16x4 matrix instruction.
 template <int D, int C>
 struct LocalLds {
+  static constexpr int NIB = C / 16;
+  static constexpr int NBLK = NIB * (NIB + 1) / 2;  // lower blocks, diagonal included
+  static constexpr int AP = 20;                     // f32 pitch of an A block row
   union {
+    uint16_t kq[2 * C * D];  // K tile, then Q tile; swizzled rows (kn_index)
     struct {
-      uint16_t K[C * Cfg<D, C>::LDK];
-      uint16_t Q[C * Cfg<D, C>::LDK];
-    } kq;
-    struct {
-      float A[C * Cfg<D, C>::LDA];
-      float linv[C / 16][16 * 17];   // transposed diagonal inverses
-      float sa[4][16 * 17], sb[4][16 * 17];
+      float A[NBLK][16 * AP];     // block (m, c) at m (m + 1) / 2 + c, row-major
+      float linv[NIB][16 * 17];   // transposed diagonal inverses
+      float gam[4][64];           // per-wavefront copies of gamma and beta
+      float bet[4][64];
     } inv;
   } u;
 };
+
+// Block rows of row set p (one row set per pair of wavefronts): the longest
+// row with the shortest, so that every set holds the same number of tiles.
+template <int NIB>
+__device__ __forceinline__ int gram_row(int p, int r) {
+  if (r == 0) return NIB - 1 - p;
+  return NIB == 4 ? p : -1;
+}
 
 template <int D, int C, typename TIn>
 __global__ __launch_bounds__(256) void chunk_local_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k,
     const float *__restrict__ g, const float *__restrict__ beta,
     const int32_t *__restrict__ cu, int n_seqs, int hqk, int hv, int group,
-    float *__restrict__ dec_ws, uint16_t *__restrict__ tfrag,
+    int n_pairs, float *__restrict__ dec_ws, uint16_t *__restrict__ tfrag,
     uint16_t *__restrict__ pfrag, uint16_t *__restrict__ qfrag,
     uint16_t *__restrict__ kcopy) {
   using F = Cfg<D, C>;
-  constexpr int NIB = F::NIB, KS = F::KS;
-  constexpr int NP = C * (D / 8);  // 16-byte row pieces of K (and of Q)
-  constexpr int NL = (NP + 255) / 256;
-  __shared__ __attribute__((aligned(16))) LocalLds<D, C> L;
-  __shared__ int owner;
+  using LL = LocalLds<D, C>;
+  constexpr int NIB = F::NIB, KS = F::KS, AP = LL::AP;
+  constexpr int NKI = C * D / 512;  // 1 KB pieces of the K (or Q) tile
+  constexpr int KPR = D / 8;        // 16-byte pieces per row
+  static_assert(NIB == 1 || NIB == 2 || NIB == 4, "row sets");
+  __shared__ __attribute__((aligned(16))) LL L;
+  uint16_t *Kt = L.u.kq, *Qt = L.u.kq + C * D;
 
-  const int cidx = blockIdx.x;
-  const int hk = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // The sequence owning slot cidx, if any (every sequence is tested once).
-  if (tid == 0) owner = -1;
-  __syncthreads();
-  for (int m = tid; m < n_seqs; m += 256) {
-    const int64_t base = first_slot(cu, m, C);
-    if (cidx >= base && cidx < base + (cu[m + 1] - cu[m] + C - 1) / C) owner = m;
-  }
-  __syncthreads();
-  const int n = owner;
-  if (n < 0) return;
-  const int64_t t0 = cu[n] + (cidx - first_slot(cu, n, C)) * C;
-  const int nvalid = (int)min((int64_t)C, (int64_t)cu[n + 1] - t0);
+  // Block id -> (chunk, key head) pair and head of the group. Work-groups are
+  // dealt to the eight XCDs round robin, so ids b and b + 8 share one: the
+  // heads of a group for one pair take ids 8 (group j + gi) + x.
+  const int bid = blockIdx.x;
+  const int xg = bid & 7, jj = bid >> 3;
+  const int gi = jj % group;
+  const int pair = (jj / group) * 8 + xg;
+  if (pair >= n_pairs) return;
+  const int cidx = pair / hqk, hk = pair - cidx * hqk;
+  const int h = hk * group + gi;
+  const int64_t slot = (int64_t)cidx * hv + h;
 
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
   const int l16 = lane & 15, g4 = lane >> 4;
-  const int ib = wave;
+
+  // ---- the sequence owning slot cidx, if any: each wavefront tests the
+  // sequences 64 at a time and takes the (single) hit from a ballot.
+  int n = -1, cu_n = 0, cu_n1 = 0;
+  for (int m0 = 0; m0 < n_seqs; m0 += 64) {
+    const int m = m0 + lane;
+    int a = 0, b = 0;
+    bool hit = false;
+    if (m < n_seqs) {
+      a = cu[m];
+      b = cu[m + 1];
+      const int64_t base = (int64_t)a / C + m;  // first_slot(cu, m, C)
+      hit = cidx >= base && cidx < base + (b - a + C - 1) / C;
+    }
+    const uint64_t bal = __ballot(hit);
+    if (bal != 0) {
+      const int src = __ffsll((unsigned long long)bal) - 1;
+      n = m0 + src;
+      cu_n = __builtin_amdgcn_readlane(a, src);
+      cu_n1 = __builtin_amdgcn_readlane(b, src);
+      break;
+    }
+  }
+  if (n < 0) return;  // an unused slot: the same for every wavefront
+  const int64_t t0 = cu_n + (cidx - ((int64_t)cu_n / C + n)) * C;
+  const int nvalid = (int)min((int64_t)C, (int64_t)cu_n1 - t0);
 
   // ---- loads: rows past the end of the sequence read as zero
   const uint32_t rowb = (uint32_t)(nvalid * hqk * D * sizeof(TIn));
@@ -134,115 +192,133 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   const rsrc_t rq = make_rsrc(q + (t0 * hqk + hk) * D, rowb);
   const rsrc_t rg = make_rsrc(g + t0 * hv, (uint32_t)(nvalid * hv * 4));
   const rsrc_t rb = make_rsrc(beta + t0 * hv, (uint32_t)(nvalid * hv * 4));
-  uint4 kv[NL], qv[NL];
+  const float gl = buf_load_f32(rg, (uint32_t)(lane * hv + h) * 4u);
+  const float bta = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
+  if constexpr (sizeof(TIn) == 2) {
+    // Buffer-to-LDS copies: lane i of a copy fills bytes [16 i, 16 i + 16) of
+    // its 1 KB piece, so the source offset picks the global 16-byte piece that
+    // belongs at that swizzled position.
 #pragma unroll
-  for (int u = 0; u < NL; ++u) {
-    const int idx = min(tid + 256 * u, NP - 1);
-    const uint32_t e = (uint32_t)((idx / (D / 8)) * hqk * D + (idx % (D / 8)) * 8);
-    kv[u] = BufElem<TIn>::load8(rk, e);
-    qv[u] = BufElem<TIn>::load8(rq, e);
-  }
-  const uint32_t grow = (uint32_t)(lane * hv + hk * group);
-  float gnext = buf_load_f32(rg, grow * 4u);
-  float bnext = buf_load_f32(rb, grow * 4u);
+    for (int it = 0; it < (2 * NKI + 3) / 4; ++it) {
+      const int m = wave + 4 * it;
+      if (m >= 2 * NKI) break;
+      const bool isq = m >= NKI;
+      const int mm = isq ? m - NKI : m;
+      const int u = 64 * mm + lane, row = u / KPR;
+      const int gp = (u % KPR) ^ kn_swizzle<D>(row);
+      const uint32_t off = (uint32_t)((row * hqk * D + 8 * gp) * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(isq ? rq : rk, (lds_void *)((isq ? Qt : Kt) + 512 * mm),
+                                               16, off, 0, 0, 0);
+    }
+  } else {
+    constexpr int NP = C * KPR;
+    constexpr int NL = (NP + 255) / 256;
+    uint4 kv[NL], qv[NL];
 #pragma unroll
-  for (int u = 0; u < NL; ++u) {
-    const int idx = tid + 256 * u;
-    if (idx < NP) {
-      const int r = idx / (D / 8), seg = idx % (D / 8);
-      *reinterpret_cast<uint4 *>(&L.u.kq.K[r * F::LDK + seg * 8]) = kv[u];
-      *reinterpret_cast<uint4 *>(&L.u.kq.Q[r * F::LDK + seg * 8]) = qv[u];
+    for (int u = 0; u < NL; ++u) {
+      const int idx = min(tid + 256 * u, NP - 1);
+      const uint32_t e = (uint32_t)((idx / KPR) * hqk * D + (idx % KPR) * 8);
+      kv[u] = BufElem<TIn>::load8(rk, e);
+      qv[u] = BufElem<TIn>::load8(rq, e);
+    }
+#pragma unroll
+    for (int u = 0; u < NL; ++u) {
+      const int idx = tid + 256 * u;
+      if (idx < NP) {
+        const int x = kn_index<D>(idx / KPR, 8 * (idx % KPR));
+        *reinterpret_cast<uint4 *>(&Kt[x]) = kv[u];
+        *reinterpret_cast<uint4 *>(&Qt[x]) = qv[u];
+      }
     }
   }
-  lds_barrier();
+  // gamma: inclusive prefix sum of g over the chunk, lane t holding token t
+  // (lanes past the end and past C hold g = 0: they repeat the last value).
+  const float gam = wave_prefix_sum(gl);
+  if (wave == 0 && lane < C) {
+    // decay factors for the carry: exp(gamma_i) and exp(gamma_last - gamma_i)
+    const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gam), C - 1));
+    dec_ws[slot * 2 * C + lane] = __expf(gam);
+    dec_ws[slot * 2 * C + C + lane] = __expf(glast - gam);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
 
   // ---- Q of this chunk for the carry, in the A-operand order of Q S^T:
   // block ib, step s, lane (l16, g4) holds Q[16 ib + l16][32 s + 8 g4 + (0..7)].
   // For f32 inputs also a bf16 copy of K, row-major [C][D], for the carry.
-  if (ib < NIB) {
+  // One value head of the group writes them.
+  if (gi == 0 && wave < NIB) {
     const int64_t base = ((int64_t)cidx * hqk + hk) * (C * D);
-    uint16_t *qf = qfrag + base + ((int64_t)ib * F::DS * 64 + lane) * 8;
+    uint16_t *qf = qfrag + base + ((int64_t)wave * F::DS * 64 + lane) * 8;
 #pragma unroll
     for (int s = 0; s < F::DS; ++s)
       *reinterpret_cast<uint4 *>(qf + s * 512) =
-          *reinterpret_cast<const uint4 *>(&L.u.kq.Q[(16 * ib + l16) * F::LDK + 32 * s + 8 * g4]);
+          *reinterpret_cast<const uint4 *>(&Qt[kn_index<D>(16 * wave + l16, 32 * s + 8 * g4)]);
     if (sizeof(TIn) == 4) {
-      uint16_t *kc = kcopy + base + (int64_t)(16 * ib + l16) * D;
+      uint16_t *kc = kcopy + base + (int64_t)(16 * wave + l16) * D;
 #pragma unroll
       for (int s = 0; s < F::DS; ++s)
         *reinterpret_cast<uint4 *>(kc + 32 * s + 8 * g4) =
-            *reinterpret_cast<const uint4 *>(&L.u.kq.K[(16 * ib + l16) * F::LDK + 32 * s + 8 * g4]);
+            *reinterpret_cast<const uint4 *>(&Kt[kn_index<D>(16 * wave + l16, 32 * s + 8 * g4)]);
     }
   }
 
-  // ---- Gram tiles for column block ib, row blocks jb <= ib. Lane (l16, g4)
-  // element e holds  k_j . k_i  and  k_j . q_i,  j = 16 jb + 4 g4 + e,
+  // ---- Gram tiles (ib, jb), jb <= ib, of this wavefront's product. Lane
+  // (l16, g4) element e holds  k_j . k_i  (or  k_j . q_i),  j = 16 jb + 4 g4 + e,
   // i = 16 ib + l16.
-  f32x4 Gk[NIB], Gq[NIB];
+  const int prod = wave & 1;
+  const int rset = wave >> 1;
+  const uint16_t *Bt = prod ? Qt : Kt;
+  int rows[2];
+  f32x4 G[2][NIB];
 #pragma unroll
-  for (int jb = 0; jb < NIB; ++jb) {
-    Gk[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    Gq[jb] = Gk[jb];
-    if (ib < NIB && jb <= ib) {
+  for (int r = 0; r < 2; ++r) {
+    rows[r] = gram_row<NIB>(rset, r);
+    const int ib = rows[r];
+#pragma unroll
+    for (int jb = 0; jb < NIB; ++jb) {
+      G[r][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (jb > ib) continue;
 #pragma unroll
       for (int s = 0; s < F::DS; ++s) {
         const int col = 32 * s + 8 * g4;
-        const uint4 a = *reinterpret_cast<const uint4 *>(&L.u.kq.K[(16 * jb + l16) * F::LDK + col]);
-        const uint4 bk = *reinterpret_cast<const uint4 *>(&L.u.kq.K[(16 * ib + l16) * F::LDK + col]);
-        const uint4 bq = *reinterpret_cast<const uint4 *>(&L.u.kq.Q[(16 * ib + l16) * F::LDK + col]);
-        Gk[jb] = mfma_16x16x32(a, bk, Gk[jb]);
-        Gq[jb] = mfma_16x16x32(a, bq, Gq[jb]);
+        const uint4 a = *reinterpret_cast<const uint4 *>(&Kt[kn_index<D>(16 * jb + l16, col)]);
+        const uint4 bb = *reinterpret_cast<const uint4 *>(&Bt[kn_index<D>(16 * ib + l16, col)]);
+        G[r][jb] = mfma_16x16x32(a, bb, G[r][jb]);
       }
     }
   }
   lds_barrier();  // the K and Q tiles are dead; the space is reused below
 
-  for (int gi = 0; gi < group; ++gi) {
-    const int h = hk * group + gi;
-    const int64_t slot = (int64_t)cidx * hv + h;
-    float gam = gnext;  // this lane's row: g (zero past the sequence end)
-    const float bta = bnext;
-    if (gi + 1 < group) {
-      gnext = buf_load_f32(rg, (grow + gi + 1) * 4u);
-      bnext = buf_load_f32(rb, (grow + gi + 1) * 4u);
-    }
+  // ---- decay masks: A (product 0) to LDS, P (product 1) to global.
+  float *gw = L.u.inv.gam[wave], *bw = L.u.inv.bet[wave];
+  gw[lane] = gam;
+  bw[lane] = bta;
+  wave_lds_fence();
 #pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {  // inclusive prefix sum: gamma
-      const float y = __shfl_up(gam, d, 64);
-      if (lane >= d) gam += y;
-    }
-    const float glast = __shfl(gam, C - 1, 64);
-    if (wave == 0 && lane < C) {
-      // decay factors for the carry: exp(gamma_i) and exp(gamma_last - gamma_i)
-      dec_ws[slot * 2 * C + lane] = __expf(gam);
-      dec_ws[slot * 2 * C + C + lane] = __expf(glast - gam);
-    }
-
-    f32x4 At[NIB], Z[NIB];
+  for (int r = 0; r < 2; ++r) {
+    const int ib = rows[r];
+    if (ib < 0) continue;
+    const int i = 16 * ib + l16;
+    const float gami = gw[i], bi = bw[i];
+    f32x4 Pt[NIB];
 #pragma unroll
     for (int jb = 0; jb < NIB; ++jb) {
-      At[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      Z[jb] = At[jb];
-    }
-    if (ib < NIB) {
-      const int i = 16 * ib + l16;
-      const float gami = __shfl(gam, i, 64), bi = __shfl(bta, i, 64);
-      f32x4 Pt[NIB];
+      Pt[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (jb > ib) continue;
+      const float4 gj = *reinterpret_cast<const float4 *>(&gw[16 * jb + 4 * g4]);
+      const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
 #pragma unroll
-      for (int jb = 0; jb < NIB; ++jb) {
-        Pt[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (jb > ib) continue;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int j = 16 * jb + 4 * g4 + e;
-          const float gamj = __shfl(gam, j, 64);
-          const float dec = (j <= i) ? __expf(gami - gamj) : 0.f;
-          Pt[jb][e] = dec * Gq[jb][e];
-          At[jb][e] = (j < i) ? bi * dec * Gk[jb][e] : 0.f;
-        }
-        *reinterpret_cast<float4 *>(&L.u.inv.A[i * F::LDA + 16 * jb + 4 * g4]) =
-            make_float4(At[jb][0], At[jb][1], At[jb][2], At[jb][3]);
+      for (int e = 0; e < 4; ++e) {
+        const int j = 16 * jb + 4 * g4 + e;
+        const float dec = (j <= i) ? __expf(gami - gjv[e]) : 0.f;
+        Pt[jb][e] = prod ? dec * G[r][jb][e] : ((j < i) ? bi * dec * G[r][jb][e] : 0.f);
       }
+      if (!prod)
+        *reinterpret_cast<float4 *>(&L.u.inv.A[ib * (ib + 1) / 2 + jb][l16 * AP + 4 * g4]) =
+            make_float4(Pt[jb][0], Pt[jb][1], Pt[jb][2], Pt[jb][3]);
+    }
+    if (prod) {
       // P as A-operand fragments: step s takes tile 2s (elements 0-3) and
       // tile 2s+1 (elements 4-7), i.e. the token order of tok_pos().
       uint16_t *pf = pfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
@@ -255,103 +331,85 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
                        pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
       }
     }
-    lds_barrier();
+  }
+  lds_barrier();
 
-    // ---- diagonal block: M = A[b][b]^T (lane element e: M[4 g4 + e][l16]).
-    if (ib < NIB) {
-      const float *Ab = &L.u.inv.A[(16 * ib) * F::LDA + 16 * ib];
-      float *sa = L.u.inv.sa[wave], *sb = L.u.inv.sb[wave];
-      const f32x4 M = At[ib];
-      f32x4 X = f32x4{0.f, 0.f, 0.f, 0.f}, M2 = X;
+  // ---- diagonal blocks by forward substitution: lane (b, c) = (g4, l16)
+  // solves (I + A[b][b]) x = e_c, i.e. column c of T[b][b], and stores it as
+  // row c of the transposed inverse.
+  if (wave == 0) {
+    const int b = min(g4, NIB - 1);  // lanes past the last block repeat it
+    const float *Ab = L.u.inv.A[b * (b + 1) / 2 + b];
+    float x[16];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) X[e] = ((4 * g4 + e) == l16 ? 1.f : 0.f) - M[e];
+    for (int i = 0; i < 16; ++i) {
+      float s0 = (i == l16) ? 1.f : 0.f, s1 = 0.f;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        M2 = mfma_16x16x4_f32(Ab[(4 * g4 + kk) * F::LDA + l16], M[kk], M2);
-      // X <- X (I + M^2); then with M^4 and M^8. The A operand of X (I - M)
-      // comes straight from the A tile.
-#pragma unroll
-      for (int e = 0; e < 4; ++e) sa[(4 * g4 + e) * 17 + l16] = M2[e];
-      wave_lds_fence();
-      f32x4 M4 = f32x4{0.f, 0.f, 0.f, 0.f};
-      f32x4 X1 = X;
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        M4 = mfma_16x16x4_f32(sa[l16 * 17 + 4 * g4 + kk], M2[kk], M4);
-        const float x0 = ((4 * g4 + kk) == l16 ? 1.f : 0.f) - Ab[(4 * g4 + kk) * F::LDA + l16];
-        X1 = mfma_16x16x4_f32(x0, M2[kk], X1);
+      for (int j = 0; j + 1 < i; j += 2) {
+        s0 -= Ab[i * AP + j] * x[j];
+        s1 -= Ab[i * AP + j + 1] * x[j + 1];
       }
-      wave_lds_fence();
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        sa[(4 * g4 + e) * 17 + l16] = M4[e];
-        sb[(4 * g4 + e) * 17 + l16] = X1[e];
-      }
-      wave_lds_fence();
-      f32x4 M8 = f32x4{0.f, 0.f, 0.f, 0.f};
-      f32x4 X2 = X1;
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        M8 = mfma_16x16x4_f32(sa[l16 * 17 + 4 * g4 + kk], M4[kk], M8);
-        X2 = mfma_16x16x4_f32(sb[l16 * 17 + 4 * g4 + kk], M4[kk], X2);
-      }
-      wave_lds_fence();
-#pragma unroll
-      for (int e = 0; e < 4; ++e) sb[(4 * g4 + e) * 17 + l16] = X2[e];
-      wave_lds_fence();
-      f32x4 X3 = X2;
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        X3 = mfma_16x16x4_f32(sb[l16 * 17 + 4 * g4 + kk], M8[kk], X3);
-      // X3 = (T[b][b])^T; publish it for the other block rows.
-#pragma unroll
-      for (int e = 0; e < 4; ++e) L.u.inv.linv[ib][(4 * g4 + e) * 17 + l16] = X3[e];
-#pragma unroll
-      for (int jb = 0; jb < NIB; ++jb)
-        if (jb == ib) Z[jb] = X3;
+      if (i & 1) s0 -= Ab[i * AP + i - 1] * x[i - 1];
+      x[i] = s0 + s1;
     }
-    lds_barrier();
+    if (g4 < NIB) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) L.u.inv.linv[b][l16 * 17 + i] = x[i];
+    }
+  }
+  lds_barrier();
 
-    // ---- block row ib, right to left: Z[c] = (T[ib][c])^T.
-    if (ib < NIB) {
+  // ---- block row ib = wave, right to left: Z[c] = (T[ib][c])^T.
+  if (wave < NIB) {
+    const int ib = wave;
+    f32x4 Z[NIB];
 #pragma unroll
-      for (int c = NIB - 2; c >= 0; --c) {
-        if (c >= ib) continue;
-        f32x4 R = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < NIB; ++c) {
+      Z[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (c == ib) {
 #pragma unroll
-        for (int m = 1; m < NIB; ++m) {
-          if (m <= c || m > ib) continue;
-          const float *Amc = &L.u.inv.A[(16 * m) * F::LDA + 16 * c];
+        for (int e = 0; e < 4; ++e) Z[c][e] = L.u.inv.linv[ib][(4 * g4 + e) * 17 + l16];
+      }
+    }
 #pragma unroll
-          for (int kk = 0; kk < 4; ++kk)
-            R = mfma_16x16x4_f32(Amc[(4 * g4 + kk) * F::LDA + l16], Z[m][kk], R);
-        }
-        f32x4 Zc = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c = NIB - 2; c >= 0; --c) {
+      if (c >= ib) continue;
+      f32x4 R = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int m = 1; m < NIB; ++m) {
+        if (m <= c || m > ib) continue;
+        const float *Amc = L.u.inv.A[m * (m + 1) / 2 + c];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk)
-          Zc = mfma_16x16x4_f32(L.u.inv.linv[c][l16 * 17 + 4 * g4 + kk], R[kk], Zc);
-        Z[c] = -Zc;
+          R = mfma_16x16x4_f32(Amc[(4 * g4 + kk) * AP + l16], Z[m][kk], R);
       }
-      // Fold beta into the factor: the carry uses T' = T diag(beta), so that
-      // U = T' (V - exp(gamma) X) needs no beta of its own.
+      f32x4 Zc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int c = 0; c < NIB; ++c) {
-        if (c > ib) continue;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) Z[c][e] *= __shfl(bta, 16 * c + 4 * g4 + e, 64);
-      }
-      // T' as A-operand fragments, same token order as P.
-      uint16_t *tf = tfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const f32x4 lo4 = Z[2 * s];
-        const f32x4 hi4 = (2 * s + 1 < NIB) ? Z[(2 * s + 1) % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
-        *reinterpret_cast<uint4 *>(tf + s * 512) =
-            make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
-                       pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
-      }
+      for (int kk = 0; kk < 4; ++kk)
+        Zc = mfma_16x16x4_f32(L.u.inv.linv[c][l16 * 17 + 4 * g4 + kk], R[kk], Zc);
+      Z[c] = -Zc;
     }
-    lds_barrier();  // A and the inverses are rewritten for the next head
+    // Fold beta into the factor: the carry uses T' = T diag(beta), so that
+    // U = T' (V - exp(gamma) X) needs no beta of its own.
+#pragma unroll
+    for (int c = 0; c < NIB; ++c) {
+      if (c > ib) continue;
+      const float4 bc = *reinterpret_cast<const float4 *>(&bw[16 * c + 4 * g4]);
+      Z[c][0] *= bc.x;
+      Z[c][1] *= bc.y;
+      Z[c][2] *= bc.z;
+      Z[c][3] *= bc.w;
+    }
+    // T' as A-operand fragments, same token order as P.
+    uint16_t *tf = tfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const f32x4 lo4 = Z[2 * s];
+      const f32x4 hi4 = (2 * s + 1 < NIB) ? Z[(2 * s + 1) % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
+      *reinterpret_cast<uint4 *>(tf + s * 512) =
+          make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
+                     pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
+    }
   }
 }
 
@@ -408,25 +466,12 @@ struct CarryLds {
   uint16_t Uh[16 * F::LDV];     // exp(gamma_last - gamma) U, same layout
 };
 
-// Element index of (row, column) in a swizzled row-major [rows][D] tile:
-// 16-byte chunks are XORed with a row function so that 16 consecutive rows
-// at one column (matrix-operand reads) fall on distinct bank groups.
-template <int D>
-__device__ __forceinline__ int kn_swizzle(int row) {
-  return ((row & 15) ^ ((row >> 4) & 3)) & (D / 8 - 1);
-}
-template <int D>
-__device__ __forceinline__ int kn_index(int row, int col) {
-  return row * D + 8 * ((col >> 3) ^ kn_swizzle<D>(row)) + (col & 7);
-}
-
 __device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) {
   return make_uint2(pack_bf16x2(a, b), pack_bf16x2(c, d));
 }
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-typedef __attribute__((address_space(3))) void lds_void;
 
 // K^T as the A operand of the state update for key tile t, token step s:
 // lane (l16, g4) gets K[j][16 t + l16] for the 8 tokens at positions
@@ -884,10 +929,13 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
 
   const int64_t nc = chunk_bound(a.n_seqs, a.n_tokens, C);
   if (a.n_tokens > 0) {
-    hipLaunchKernelGGL((chunk_local_kernel<D, C, TIn>), dim3((unsigned)nc, (unsigned)a.hqk),
-                       dim3(256), 0, a.stream, (const TIn *)a.q, (const TIn *)a.k,
-                       a.g, a.beta, a.cu_seqlens, a.n_seqs, a.hqk, a.hv, group, dec,
-                       tf, pf, qf, kc);
+    // (chunk, key head) pairs in groups of eight, times the heads of a group.
+    const int64_t pairs = nc * a.hqk;
+    const int64_t lblocks = ((pairs + 7) / 8) * 8 * group;
+    hipLaunchKernelGGL((chunk_local_kernel<D, C, TIn>), dim3((unsigned)lblocks), dim3(256), 0,
+                       a.stream, (const TIn *)a.q, (const TIn *)a.k, a.g, a.beta,
+                       a.cu_seqlens, a.n_seqs, a.hqk, a.hv, group, (int)pairs, dec, tf, pf,
+                       qf, kc);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
