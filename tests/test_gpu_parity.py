@@ -183,6 +183,19 @@ def test_prefill_alias_in_place():
     check_full("alias", synth.make(w), dev, alias=True)
 
 
+@pytest.mark.parametrize("alias", [False, True])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_prefill_ragged_c16(alias, dtype):
+    """Ragged batch at C = 16 (30 chunk slots): long and short sequences, an
+    empty one, a nonzero initial state, also updated in place."""
+    dev = require_gpu()
+    w = synth.PREFILL_4K.replace(seq_len=None, lengths=(150, 0, 33, 200, 5), n_seqs=5,
+                                 hqk=2, hv=4, d=64, dtype=dtype, g_mu=-4.0,
+                                 state_std=0.1, seed=53)
+    check_full("ragged_c16_alias%d_%s" % (alias, dtype), synth.make(w), dev, chunk=16,
+               alias=alias)
+
+
 def test_prefill_group4_and_group1():
     dev = require_gpu()
     for hqk, hv in ((2, 8), (4, 4)):
