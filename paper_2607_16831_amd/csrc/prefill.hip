@@ -640,12 +640,14 @@ struct StateTile {
   __device__ __forceinline__ void update(CarryLds<D, C, TIn> &L, f32x4 &S, int b, int wave,
                                          int l16, int g4) {
     using F = Cfg<D, C>;
-    f32x4 acc = S * L.Dl[b][C - 1];
+    uint4 bu[F::KS];
 #pragma unroll
-    for (int s = 0; s < F::KS; ++s) {
-      const uint4 bu = *reinterpret_cast<const uint4 *>(&L.Uh[l16 * F::LDV + 32 * s + 8 * g4]);
-      acc = mfma_16x16x32(kt[s], bu, acc);
-    }
+    for (int s = 0; s < F::KS; ++s)
+      bu[s] = *reinterpret_cast<const uint4 *>(&L.Uh[l16 * F::LDV + 32 * s + 8 * g4]);
+    f32x4 acc = S * L.Dl[b][C - 1];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < F::KS; ++s) acc = mfma_16x16x32(kt[s], bu[s], acc);
     S = acc;
     *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
         pack4_bf16(acc[0], acc[1], acc[2], acc[3]);
@@ -686,29 +688,38 @@ __device__ __forceinline__ void carry_compute_xu(
       const float4 ge4 = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
       const float4 he4 = *reinterpret_cast<const float4 *>(&L.Dl[b][C + tb]);
       he[0] = he4.x; he[1] = he4.y; he[2] = he4.z; he[3] = he4.w;
-      f32x4 xs = f32x4{0.f, 0.f, 0.f, 0.f};
+      // every operand read of a phase is issued before its first product
+      uint4 bs[F::DS], ka[F::DS];
 #pragma unroll
       for (int s = 0; s < F::DS; ++s) {
-        const uint4 bs = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
-        const uint4 a = *reinterpret_cast<const uint4 *>(&L.Kn[b][kn_index<D>(16 * ib + l16, 32 * s + 8 * g4)]);
-        xs = mfma_16x16x32(a, bs, xs);
+        bs[s] = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
+        ka[s] = *reinterpret_cast<const uint4 *>(&L.Kn[b][kn_index<D>(16 * ib + l16, 32 * s + 8 * g4)]);
       }
       const TIn *vt = reinterpret_cast<const TIn *>(L.Vl[b]);
+      float vv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) vv[e] = Elem<TIn>::load1(&vt[(tb + e) * 16 + l16]);
+      __builtin_amdgcn_sched_barrier(0);
+      f32x4 xs = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < F::DS; ++s) xs = mfma_16x16x32(ka[s], bs[s], xs);
       const float ge[4] = {ge4.x, ge4.y, ge4.z, ge4.w};
       float y[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) y[e] = Elem<TIn>::load1(&vt[(tb + e) * 16 + l16]) - ge[e] * xs[e];
+      for (int e = 0; e < 4; ++e) y[e] = vv[e] - ge[e] * xs[e];
       *reinterpret_cast<uint2 *>(&L.Yl[l16 * F::LDV + ypos]) = pack4_bf16(y[0], y[1], y[2], y[3]);
     }
     lds_barrier();
     // ---- phase 2: U = T' Y and exp(gamma_last - gamma) U
     if (blk) {
+      uint4 by[F::KS];
+#pragma unroll
+      for (int s = 0; s < F::KS; ++s)
+        by[s] = *reinterpret_cast<const uint4 *>(&L.Yl[l16 * F::LDV + 32 * s + 8 * g4]);
+      __builtin_amdgcn_sched_barrier(0);
       f32x4 u = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < F::KS; ++s) {
-        const uint4 by = *reinterpret_cast<const uint4 *>(&L.Yl[l16 * F::LDV + 32 * s + 8 * g4]);
-        u = mfma_16x16x32(fa[s], by, u);
-      }
+      for (int s = 0; s < F::KS; ++s) u = mfma_16x16x32(fa[s], by[s], u);
       *reinterpret_cast<uint2 *>(&L.Ul[l16 * F::LDV + ypos]) = pack4_bf16(u[0], u[1], u[2], u[3]);
       *reinterpret_cast<uint2 *>(&L.Uh[l16 * F::LDV + ypos]) =
           pack4_bf16(he[0] * u[0], he[1] * u[1], he[2] * u[2], he[3] * u[3]);
@@ -751,12 +762,14 @@ __device__ __forceinline__ void carry_compute_o(
     return make_rsrc(qfrag + ((c0 + lc) * hqk + hk) * (C * D), C * D * 2);
   };
   auto out = [&](int bb, const uint4 *pa, const f32x4 &qs, const float *gq) {
+    uint4 bu[F::KS];
+#pragma unroll
+    for (int s = 0; s < F::KS; ++s)
+      bu[s] = *reinterpret_cast<const uint4 *>(&L.Ul[l16 * F::LDV + 32 * s + 8 * g4]);
+    __builtin_amdgcn_sched_barrier(0);
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < F::KS; ++s) {
-      const uint4 bu = *reinterpret_cast<const uint4 *>(&L.Ul[l16 * F::LDV + 32 * s + 8 * g4]);
-      acc = mfma_16x16x32(pa[s], bu, acc);
-    }
+    for (int s = 0; s < F::KS; ++s) acc = mfma_16x16x32(pa[s], bu[s], acc);
     TIn *ot = reinterpret_cast<TIn *>(L.Ol[bb]);
 #pragma unroll
     for (int e = 0; e < 4; ++e) Elem<TIn>::store1(&ot[(tb + e) * 16 + l16], gq[e] * qs[e] + acc[e]);
@@ -787,12 +800,14 @@ __device__ __forceinline__ void carry_compute_o(
     lds_barrier();
     // ---- phase 2: Q S^T (S is still the state entering chunk lc)
     if (blk) {
+      uint4 bs[F::DS];
+#pragma unroll
+      for (int s = 0; s < F::DS; ++s)
+        bs[s] = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
+      __builtin_amdgcn_sched_barrier(0);
       f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < F::DS; ++s) {
-        const uint4 bs = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
-        x = mfma_16x16x32(qf[s], bs, x);
-      }
+      for (int s = 0; s < F::DS; ++s) x = mfma_16x16x32(qf[s], bs[s], x);
       qs = x;
       const float4 g4v = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
       gq[0] = g4v.x; gq[1] = g4v.y; gq[2] = g4v.z; gq[3] = g4v.w;
