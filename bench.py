@@ -15,8 +15,11 @@ fixed algorithmic counts:
   prefill bytes = T (2 HQK d e + 2 HV d e + 8 HV) + N HV d^2 4 (1 + [S0])
                   + 4 (N + 1)
   decode bytes  = 2 B HV d^2 4 + B (2 HQK + 2 HV) d 2 + 8 B HV
+`traffic` is the counter-measured byte count per launch (see MEASURED_TRAFFIC).
 """
 import argparse
+import glob
+import hashlib
 import json
 import os
 import platform
@@ -29,6 +32,27 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 matrix peak
 METRIC = "prefill tokens/sec + MFMA util; decode µs/step + achieved HBM GB/s"
+
+
+# Bytes moved per launch as the memory counters read them (FETCH_SIZE and
+# WRITE_SIZE passes, each scaled by what the counter reads for a copy of known
+# size; profiles/prefill4k_decode64_memory_counters.md), keyed by a hash of
+# the kernel sources they were taken on. Any change to those sources makes
+# the figures stale, and `traffic` is then reported as null.
+MEASURED_TRAFFIC = {
+    "b3355b1710a7aed7ebc0c5d555e0ae6677eb87d361dc344748a2300b183fcec4":
+        {"prefill": 264594806, "decode": 274390773},
+}
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_16831_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def prefill_flops(T, hqk, hv, d, C):
@@ -52,6 +76,10 @@ def main():
     ap.add_argument("--rotate", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
+                    help="before warm-up, run a read-once/write-once kernel over MB "
+                         "megabytes (three times), whose memory counters calibrate "
+                         "FETCH_SIZE / WRITE_SIZE")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only (the recurrence has no "
@@ -82,6 +110,15 @@ def main():
         t["o"] = torch.empty((wd.n_seqs, wd.hv, wd.d), dtype=torch.bfloat16, device=dev)
         D.append(t)
     torch.cuda.synchronize()
+
+    if args.copy_calibration > 0:
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)  # reads n*4 bytes, writes n*4 bytes
+        torch.cuda.synchronize()
+        del src, dst
 
     def run_prefill(s):
         gdn.prefill(s["q"], s["k"], s["v"], s["g"], s["beta"], s["cu_seqlens"],
@@ -126,15 +163,18 @@ def main():
     pre_tflops = flop / pre_avg / 1e12
     dec_gbs = dbytes / dec_avg / 1e9
 
+    measured = MEASURED_TRAFFIC.get(kernel_source_hash())
     roof_pre = {"bound": "mfma", "achieved": round(pre_tflops, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4),
+                "traffic": measured["prefill"] if measured else None,
                 "kernel": "gdn_prefill (chunk_local + chunk_carry)",
                 "algorithmic_flop_per_launch": flop,
                 "hbm_view_gbs": round(pbytes / pre_avg / 1e9, 1)}
     roof_dec = {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(dec_gbs / PEAK_HBM_GBS, 4),
-                "traffic": None, "kernel": "decode_kernel<128, bf16>",
+                "traffic": measured["decode"] if measured else None,
+                "kernel": "decode_kernel<128, bf16>",
                 "algorithmic_bytes_per_launch": dbytes}
     dominant = roof_dec if dec_avg >= pre_avg else roof_pre
 
