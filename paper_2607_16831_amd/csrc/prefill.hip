@@ -443,10 +443,11 @@ struct CarryCfg {
   static constexpr int VPR = ESZ;                // 16-byte units per token of a V/O tile row
   static constexpr int VU = C * VPR;             // 16-byte units of the V (or O) tile
   static constexpr int NVI = (VU + 63) / 64;     // 1 KB copies per V tile
-  static constexpr int NDI = (2 * C + 63) / 64;  // 256-byte copies of the 2C decay factors
+  static constexpr int NDI = (2 * C + 255) / 256;  // 1 KB copies of the 2C decay factors
   static constexpr int M = NKI + NVI + NDI;      // copies per chunk
   static constexpr int SLOTS = (M + NLW - 1) / NLW;
   static constexpr int NOU = (VU + 64 * NLW - 1) / (64 * NLW);  // output units per loader lane
+  static constexpr int NB = 3;                   // LDS buffers of the copied inputs
   static_assert(NT == 640, "launch bounds of the carry kernel");
 };
 
@@ -456,10 +457,12 @@ template <int D, int C, typename TIn>
 struct CarryLds {
   using F = Cfg<D, C>;
   using CC = CarryCfg<D, C, TIn>;
-  uint16_t Kn[2][F::CP * D];    // K chunk, row-major, swizzled; rows C..CP-1 stay zero
-  uint4 Vl[2][CC::NVI * 64];    // V tile, [token][16 values], input element type
-  uint4 Ol[2][CC::NVI * 64];    // output tile, same layout
-  float Dl[2][CC::NDI * 64];    // exp(gamma_i), then exp(gamma_last - gamma_i)
+  // The copied inputs of chunk lc live in buffer lc % NB; the output tile of
+  // chunk lc is staged in Ol[lc & 1].
+  uint16_t Kn[CC::NB][F::CP * D];  // K chunk, row-major, swizzled; rows C..CP-1 stay zero
+  uint4 Vl[CC::NB][CC::NVI * 64];  // V tile, [token][16 values], input element type
+  uint4 Ol[2][CC::NVI * 64];       // output tile, same layout
+  float Dl[CC::NB][CC::NDI * 256];  // exp(gamma_i), then exp(gamma_last - gamma_i)
   uint16_t Sl[16 * F::LDK];     // bf16 copy of the state tile, [value][key]
   uint16_t Yl[16 * F::LDV];     // Y,  [value][token position]
   uint16_t Ul[16 * F::LDV];     // U,  [value][token position]
@@ -496,8 +499,8 @@ __device__ __forceinline__ uint4 kt_operand(const uint16_t *Kn, int t, int s,
 constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond every resource: reads 0
 
 // ---------------------------------------------------------------- loaders
-// Copy m of a chunk, in order: K (1 KB each), V tile (1 KB each), decay
-// factors (256 bytes each). A buffer-to-LDS load writes lane i's bytes at
+// Copy m of a chunk, in order: K, V tile, decay factors, each 16 bytes per
+// lane (1 KB per copy). A buffer-to-LDS load writes lane i's bytes at
 // LDS base + i * size, so the per-lane source offset chooses what lands
 // where: for K it undoes the row swizzle. The offsets do not change from
 // chunk to chunk.
@@ -513,8 +516,8 @@ __device__ __forceinline__ uint32_t copy_offset(int m, int lane, int kstride, in
     if (u >= CC::VU) return kOutOfRange;
     return (uint32_t)(((u / CC::VPR) * hv * D + (u % CC::VPR) * (16 / CC::ESZ)) * CC::ESZ);
   } else if (m < CC::M) {
-    const int u = 64 * (m - CC::NKI - CC::NVI) + lane;
-    return u < 2 * C ? (uint32_t)(4 * u) : kOutOfRange;
+    const int u = 64 * (m - CC::NKI - CC::NVI) + lane;  // 4 factors per lane
+    return 4 * u < 2 * C ? (uint32_t)(16 * u) : kOutOfRange;
   }
   return kOutOfRange;
 }
@@ -532,7 +535,7 @@ __device__ __forceinline__ void issue_copy(CarryLds<D, C, TIn> &L, int bb, const
   } else if (m < CC::NKI + CC::NVI) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(R.v, (lds_void *)&L.Vl[bb][64 * (m - CC::NKI)], 16, off, 0, 0, 0);
   } else if (m < CC::M) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(R.d, (lds_void *)&L.Dl[bb][64 * (m - CC::NKI - CC::NVI)], 4, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(R.d, (lds_void *)&L.Dl[bb][256 * (m - CC::NKI - CC::NVI)], 16, off, 0, 0, 0);
   }
 }
 
@@ -551,8 +554,35 @@ __device__ __forceinline__ void store_out(const CarryLds<D, C, TIn> &L, int bb, 
   }
 }
 
+// Copies loader LW issues per chunk, and output stores it issues per chunk
+// (a store instruction is issued when its first lane is in range).
+template <int D, int C, typename TIn, int LW>
+constexpr int loader_copies() {
+  using CC = CarryCfg<D, C, TIn>;
+  int n = 0;
+  for (int i = 0; i < CC::SLOTS; ++i) n += (CC::NLW * i + LW < CC::M) ? 1 : 0;
+  return n;
+}
+template <int D, int C, typename TIn, int LW>
+constexpr int loader_stores() {
+  using CC = CarryCfg<D, C, TIn>;
+  int n = 0;
+  for (int j = 0; j < CC::NOU; ++j) n += (64 * (LW + CC::NLW * j) < CC::VU) ? 1 : 0;
+  return n;
+}
+
+// Waits until at most N of this wavefront's vector-memory operations are
+// outstanding (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 // Loader wavefront LW (a template parameter, so that the kind of each of its
-// copies is known when compiling).
+// copies is known when compiling). The copies of chunk lc + 2 are issued
+// while the compute wavefronts work on chunk lc, and only those of chunk
+// lc + 1 must have landed by the end of chunk lc; the output stores are never
+// waited for (their data is read out of LDS when they issue).
 template <int D, int C, typename TIn, int LW>
 __device__ __forceinline__ void carry_loader(
     CarryLds<D, C, TIn> &L, int lane, const uint16_t *__restrict__ ksrc, int kstride,
@@ -590,26 +620,37 @@ __device__ __forceinline__ void carry_loader(
     return make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * CC::ESZ));
   };
 
-  {  // chunk 0 into buffer 0
-    const CopyRes R = res(0);
+  constexpr int NCP = loader_copies<D, C, TIn, LW>();
+  constexpr int NST = loader_stores<D, C, TIn, LW>();
+  constexpr int NA = CC::NB - 1;  // chunks in flight ahead of the one in use
+  auto issue = [&](int lc) {      // chunk lc into buffer lc % NB
+    const CopyRes R = res(lc);
 #pragma unroll
-    for (int i = 0; i < NS; ++i) issue_copy<D, C, TIn>(L, 0, R, CC::NLW * i + LW, off[i]);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
+    for (int i = 0; i < NS; ++i) issue_copy<D, C, TIn>(L, lc % CC::NB, R, CC::NLW * i + LW, off[i]);
+  };
+#pragma unroll
+  for (int j = 0; j < NA; ++j)
+    if (j < nch) issue(j);
+  if (nch >= NA)
+    wait_vm<(NA - 1) * NCP>();  // chunk 0 has landed
+  else
+    wait_vm<0>();
   lds_barrier();
 
   for (int lc = 0; lc < nch; ++lc) {
     // output of chunk lc - 2 (staged during phase 1 of chunk lc - 1), then
-    // chunk lc + 1 into the buffer chunk lc - 1 used
+    // chunk lc + NA into the buffer chunk lc - 1 used
     store_out<D, C, TIn>(L, lc & 1, out_res(max(lc - 2, 0), lc >= 2), op, ooff);
-    if (lc + 1 < nch) {
-      const CopyRes R = res(lc + 1);
-#pragma unroll
-      for (int i = 0; i < NS; ++i) issue_copy<D, C, TIn>(L, (lc & 1) ^ 1, R, CC::NLW * i + LW, off[i]);
-    }
+    if (lc + NA < nch) issue(lc + NA);
     lds_barrier();
     lds_barrier();
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // Chunk lc + 1 must have landed before the last barrier of chunk lc. In
+    // the steady state NA - 1 later iterations' stores and copies are still
+    // allowed in flight; near either end everything is waited for.
+    if (lc >= NA - 2 && lc + NA < nch)
+      wait_vm<(NA - 1) * (NST + NCP)>();
+    else
+      wait_vm<0>();
     lds_barrier();
   }
   // outputs of the last two chunks
@@ -681,7 +722,7 @@ __device__ __forceinline__ void carry_compute_xu(
   }
   StateTile<D, C, TIn> st;
   for (int lc = 0; lc < nch; ++lc) {
-    const int b = lc & 1;
+    const int b = lc % CarryCfg<D, C, TIn>::NB;  // input buffer of chunk lc
     // ---- phase 1: X = K S^T, Y = V - exp(gamma) X (beta is folded into T')
     float he[4];
     if (blk) {
@@ -787,11 +828,11 @@ __device__ __forceinline__ void carry_compute_o(
   }
   StateTile<D, C, TIn> st;
   for (int lc = 0; lc < nch; ++lc) {
-    const int b = lc & 1;
+    const int b = lc % CarryCfg<D, C, TIn>::NB;  // input buffer of chunk lc
     // ---- phase 1: output of chunk lc - 1 (for lc = 0 a zero tile into a
     // buffer nothing stores), then P of this chunk
     if (blk) {
-      out(b ^ 1, pa, qs, gq);
+      out((lc & 1) ^ 1, pa, qs, gq);
       __builtin_amdgcn_sched_barrier(0);
       const rsrc_t rp = p_res(lc);
 #pragma unroll
@@ -877,8 +918,8 @@ __global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
           L.Uh[idx] = 0;
         }
         for (int idx = C * D + tid; idx < F::CP * D; idx += 64 * CC::NCW) {
-          L.Kn[0][idx] = 0;
-          L.Kn[1][idx] = 0;
+#pragma unroll
+          for (int bb = 0; bb < CC::NB; ++bb) L.Kn[bb][idx] = 0;
         }
       }
       if (own)
