@@ -875,20 +875,22 @@ __global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
     const uint16_t *__restrict__ tfrag, const uint16_t *__restrict__ pfrag,
     const uint16_t *__restrict__ qfrag, const uint16_t *__restrict__ kcopy,
     const float *s0, float *sT, TIn *__restrict__ o, int hqk, int hv, int group,
-    int n_pairs) {
+    int n_groups) {
   using F = Cfg<D, C>;
   using CC = CarryCfg<D, C, TIn>;
   __shared__ __attribute__((aligned(16))) CarryLds<D, C, TIn> L;
 
   // Work-groups are dealt to the 8 XCDs round-robin by id. Give each XCD
-  // whole (sequence, head) pairs with their value tiles adjacent, so the
-  // tiles that share K, Q, T and P share one L2.
+  // whole (sequence, key head) groups, every value head of the group with
+  // all its value tiles, so the tiles that share K and Q (the group) and T'
+  // and P (one head) share one L2.
   const int Lb = blockIdx.x;
-  const int jx = Lb >> 3;
-  const int pair = (jx / F::NVT) * 8 + (Lb & 7);
-  const int vt = jx % F::NVT;
-  if (pair >= n_pairs) return;
-  const int n = pair / hv, h = pair % hv, hk = h / group;
+  const int jx = Lb >> 3;  // index among the work-groups of XCD Lb % 8
+  const int gq = (jx / (group * F::NVT)) * 8 + (Lb & 7);  // sequence * hqk + key head
+  const int gi = (jx / F::NVT) % group, vt = jx % F::NVT;
+  if (gq >= n_groups) return;
+  const int n = gq / hqk, hk = gq % hqk, h = hk * group + gi;
+  const int pair = n * hv + h;
   const int v0 = 16 * vt;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -996,12 +998,12 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
     if (e != hipSuccess) return e;
   }
 
-  const int n_pairs = a.n_seqs * a.hv;
-  const int64_t blocks = (int64_t)8 * ((n_pairs + 7) / 8) * F::NVT;
+  const int n_groups = a.n_seqs * a.hqk;
+  const int64_t blocks = (int64_t)8 * ((n_groups + 7) / 8) * group * F::NVT;
   hipLaunchKernelGGL((chunk_carry_kernel<D, C, TIn>), dim3((unsigned)blocks),
                      dim3(kCarryThreads), 0, a.stream, (const TIn *)a.k, (const TIn *)a.v,
                      a.cu_seqlens, dec, tf, pf, qf, kc, a.initial_state, a.final_state,
-                     (TIn *)a.o, a.hqk, a.hv, group, n_pairs);
+                     (TIn *)a.o, a.hqk, a.hv, group, n_groups);
   return hipGetLastError();
 }
 
