@@ -324,6 +324,7 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
       uint16_t *pf = pfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
+        if (2 * s > ib) continue;  // above the diagonal: zero, never stored or read
         const f32x4 lo4 = Pt[2 * s];
         const f32x4 hi4 = (2 * s + 1 < NIB) ? Pt[(2 * s + 1) % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
         *reinterpret_cast<uint4 *>(pf + s * 512) =
@@ -404,6 +405,7 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     uint16_t *tf = tfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
+      if (2 * s > ib) continue;  // above the diagonal: zero, never stored or read
       const f32x4 lo4 = Z[2 * s];
       const f32x4 hi4 = (2 * s + 1 < NIB) ? Z[(2 * s + 1) % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
       *reinterpret_cast<uint4 *>(tf + s * 512) =
@@ -708,6 +710,9 @@ __device__ __forceinline__ void carry_compute_xu(
   const bool blk = (F::NIB == 4) || (ib < F::NIB);
   const bool own = (F::NKT == 8) || (wave < F::NKT);
   const int ibc = min(ib, F::NIB - 1);
+  // T' fragments of block ibc on or below the diagonal; the others are zero,
+  // never stored, and read through an offset past the resource (zeros).
+  const int nks = min(ibc / 2 + 1, F::KS);
   const int tb = 16 * ibc + 4 * g4;                     // this lane's first token
   const int ypos = 32 * (ib >> 1) + 8 * g4 + 4 * (ib & 1);  // tok_pos(16 ib + 4 g4)
   const uint32_t foff = (uint32_t)(((ibc * F::KS) * 64 + lane) * 16);
@@ -718,7 +723,7 @@ __device__ __forceinline__ void carry_compute_xu(
   {
     const rsrc_t rt = frag_res(0);
 #pragma unroll
-    for (int s = 0; s < F::KS; ++s) fa[s] = buf_load_b128(rt, foff + 1024u * s);
+    for (int s = 0; s < F::KS; ++s) fa[s] = buf_load_b128(rt, s < nks ? foff + 1024u * s : kOutOfRange);
   }
   StateTile<D, C, TIn> st;
   for (int lc = 0; lc < nch; ++lc) {
@@ -768,7 +773,7 @@ __device__ __forceinline__ void carry_compute_xu(
       __builtin_amdgcn_sched_barrier(0);
       const rsrc_t rt = frag_res(min(lc + 1, nch - 1));
 #pragma unroll
-      for (int s = 0; s < F::KS; ++s) fa[s] = buf_load_b128(rt, foff + 1024u * s);
+      for (int s = 0; s < F::KS; ++s) fa[s] = buf_load_b128(rt, s < nks ? foff + 1024u * s : kOutOfRange);
     }
     if (own) st.fetch(L, b, wave, l16, g4);
     lds_barrier();
@@ -793,6 +798,7 @@ __device__ __forceinline__ void carry_compute_o(
   const bool blk = (F::NIB == 4) || (ib < F::NIB);
   const bool own = (F::NKT == 8) || (wave < F::NKT);
   const int ibc = min(ib, F::NIB - 1);
+  const int nks = min(ibc / 2 + 1, F::KS);  // P fragments on or below the diagonal, as T'
   const int tb = 16 * ibc + 4 * g4;
   const uint32_t foff = (uint32_t)(((ibc * F::KS) * 64 + lane) * 16);
   const uint32_t qoff = (uint32_t)(((ibc * F::DS) * 64 + lane) * 16);
@@ -836,7 +842,7 @@ __device__ __forceinline__ void carry_compute_o(
       __builtin_amdgcn_sched_barrier(0);
       const rsrc_t rp = p_res(lc);
 #pragma unroll
-      for (int s = 0; s < F::KS; ++s) pa[s] = buf_load_b128(rp, foff + 1024u * s);
+      for (int s = 0; s < F::KS; ++s) pa[s] = buf_load_b128(rp, s < nks ? foff + 1024u * s : kOutOfRange);
     }
     lds_barrier();
     // ---- phase 2: Q S^T (S is still the state entering chunk lc)
