@@ -228,6 +228,29 @@ def test_prefill_split_composition():
     assert eo <= O_BAR and es <= STATE_BAR
 
 
+@pytest.mark.parametrize("chunk", [16, 64])
+def test_prefill_poisoned_workspace(chunk):
+    """Every workspace byte set to 0xFF (NaN in bf16 and fp32) before the
+    call: a table entry read without having been written this call (such as
+    a fragment above the diagonal) would turn the output into NaN."""
+    dev = require_gpu()
+    w = synth.PREFILL_4K.replace(seq_len=None, lengths=(200, 1, 64, 130), n_seqs=4,
+                                 hqk=2, hv=4, g_mu=-3.0, state_std=0.1, seed=57)
+    x = synth.make(w)
+    d = to_dev(x, dev)
+    T = int(x["cu_seqlens"][-1])
+    ws = gdn.alloc_workspace(w.n_seqs, T, w.hqk, w.hv, w.d, chunk, dev)
+    ws.fill_(0xFF)
+    o, sT = gdn.prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], d["cu_seqlens"],
+                        initial_state=d["initial_state"], chunk=chunk, workspace=ws)
+    torch.cuda.synchronize()
+    o_ref, s_ref = oracle_prefill(x)
+    eo, es = rel_l2(o.cpu(), o_ref), rel_l2(sT.cpu(), s_ref)
+    _log("poisoned_ws_C%d" % chunk, o=eo, state=es)
+    assert torch.isfinite(o.float()).all() and torch.isfinite(sT).all()
+    assert eo <= O_BAR and es <= STATE_BAR
+
+
 def test_prefill_all_empty():
     dev = require_gpu()
     s0 = torch.randn(3, 4, 128, 128, device=dev)
