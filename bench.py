@@ -76,6 +76,8 @@ def main():
     ap.add_argument("--rotate", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-decode-sweep", action="store_true",
+                    help="skip the small-batch decode latency sweep")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="before warm-up, run a read-once/write-once kernel over MB "
                          "megabytes (three times), whose memory counters calibrate "
@@ -196,6 +198,37 @@ def main():
         "rooflines": [roof_pre, roof_dec],
     }
 
+    # ---------------------------------------------------- small-batch decode
+    # Latency of one decode step per batch size (same heads and d): K steps
+    # are captured in a HIP graph and replayed, so the time per step is the
+    # kernel's, without the host launch path of the Python binding.
+    if not args.no_decode_sweep:
+        lat = {}
+        for B in (1, 8, 16, 48, 64):
+            w = wd.replace(n_seqs=B, seed=wd.seed + 7)
+            y = synth.make(w)
+            t = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in y.items()}
+            t["o"] = torch.empty((B, w.hv, w.d), dtype=torch.bfloat16, device=dev)
+            for _ in range(3):
+                run_decode(t)
+            torch.cuda.synchronize()
+            graph, KG = torch.cuda.CUDAGraph(), 20
+            with torch.cuda.graph(graph):
+                for _ in range(KG):
+                    run_decode(t)
+            graph.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            R = 5
+            e0.record()
+            for _ in range(R):
+                graph.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            lat[str(B)] = round(e0.elapsed_time(e1) * 1e3 / (R * KG), 2)
+            del graph
+        out["decode_latency_us"] = lat
+
     # ---------------------------------------------------------------- oracle
     if not args.no_cpu_baseline:
         import oracle
@@ -206,7 +239,7 @@ def main():
                            x["initial_state"])
             reps += 1
             el = time.perf_counter() - t0
-            if el >= args.cpu_seconds or reps >= 20:
+            if el >= args.cpu_seconds:
                 break
         out["cpu_baseline"] = {
             "value": round(reps * T / el, 1), "unit": "tokens/s",

@@ -126,6 +126,43 @@ gdn_status gdn_decode(const void *q, const void *k, const void *v,
                       int32_t dk, int32_t dv, gdn_dtype dtype,
                       hipStream_t stream);
 
+/*
+ * Gate activation (paper, Section 3.2, the first two lines of the one-pass
+ * form: the multiplicative gate exp(-exp(A_log) softplus(a + b_dt)) and
+ * beta = sigmoid(b)). The *_gated entry points take the raw per-token inputs
+ * instead of g and beta and form them inside the kernels, per token t and
+ * value head h:
+ *
+ *     g[t, h]    = -exp(A_log[h]) * softplus(a[t, h] + dt_bias[h])
+ *     beta[t, h] = 1 / (1 + exp(-b[t, h]))
+ *
+ * with softplus(x) = log(1 + exp(x)); g is the log of the paper's gate, as
+ * everywhere in this header. Layouts (float32, row-major):
+ *   a, b              [T_total, HV]   (decode: [B, HV])
+ *   A_log, dt_bias    [HV]
+ * Everything else -- the other arguments, ownership, execution, errors and
+ * the workspace (gdn_prefill_workspace_size) -- is as for gdn_prefill and
+ * gdn_decode. A NULL a, b, A_log or dt_bias is GDN_ERR_INVALID_ARG when there
+ * is at least one token.
+ */
+gdn_status gdn_prefill_gated(const void *q, const void *k, const void *v,
+                             const float *a, const float *b,
+                             const float *A_log, const float *dt_bias,
+                             const int32_t *cu_seqlens,
+                             const float *initial_state, void *o,
+                             float *final_state, int32_t n_seqs,
+                             int64_t n_tokens, int32_t hqk, int32_t hv,
+                             int32_t dk, int32_t dv, int32_t chunk,
+                             gdn_dtype dtype, void *workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+gdn_status gdn_decode_gated(const void *q, const void *k, const void *v,
+                            const float *a, const float *b,
+                            const float *A_log, const float *dt_bias,
+                            float *state, void *o, int32_t batch, int32_t hqk,
+                            int32_t hv, int32_t dk, int32_t dv,
+                            gdn_dtype dtype, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

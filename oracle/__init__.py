@@ -15,7 +15,10 @@ Pins: every function here is checked in ``tests/test_oracle_pins.py`` against
 the explicit matrix form S_t = alpha S (I - beta k k^T) + beta v k^T, the
 paper's one-pass output rewrite, closed forms (beta = 0 decay, key replacement
 with orthonormal keys), exact rational arithmetic and an independent chunked
-fp64 evaluation.
+fp64 evaluation; the gate activation against numpy's logaddexp and scipy's
+expit, exact values (softplus(0) = ln 2, sigmoid(0) = 1/2), the identities
+softplus(x) - softplus(-x) = x and sigmoid(x) + sigmoid(-x) = 1, and its
+limits (A_log -> -inf gives no decay).
 """
 from __future__ import annotations
 
@@ -64,6 +67,8 @@ def _load():
             lib.gdn_ref_decode.argtypes = [dp, dp, dp, dp, dp, dp, dp,
                                            i32, i32, i32, i32, i32]
             lib.gdn_ref_decode.restype = ctypes.c_int
+            lib.gdn_ref_gate.argtypes = [dp, dp, dp, dp, dp, dp, i64, i32]
+            lib.gdn_ref_gate.restype = ctypes.c_int
             lib.gdn_ref_num_threads.argtypes = []
             lib.gdn_ref_num_threads.restype = ctypes.c_int
             _lib = lib
@@ -142,3 +147,36 @@ def decode(q, k, v, g, beta, state):
     if rc != 0:
         raise ValueError("oracle.decode: rejected arguments (code %d)" % rc)
     return o, s
+
+
+def gate(a, b, a_log, dt_bias):
+    """Gate activation of the raw inputs (paper, Section 3.2, see gdn_ref.c).
+
+    a, b: [T, HV]; a_log, dt_bias: [HV]. Returns (g, beta), both [T, HV]
+    float64: g = -exp(A_log) softplus(a + dt_bias) (the log of the paper's
+    gate), beta = sigmoid(b).
+    """
+    lib = _load()
+    a, b, a_log, dt_bias = (_f64(x) for x in (a, b, a_log, dt_bias))
+    T, HV = a.shape
+    if b.shape != (T, HV) or a_log.shape != (HV,) or dt_bias.shape != (HV,):
+        raise ValueError("oracle.gate: inconsistent shapes")
+    g = np.zeros((T, HV), dtype=np.float64)
+    beta = np.zeros((T, HV), dtype=np.float64)
+    rc = lib.gdn_ref_gate(_ptr(a), _ptr(b), _ptr(a_log), _ptr(dt_bias), _ptr(g),
+                          _ptr(beta), T, HV)
+    if rc != 0:
+        raise ValueError("oracle.gate: rejected arguments (code %d)" % rc)
+    return g, beta
+
+
+def prefill_gated(q, k, v, a, b, a_log, dt_bias, cu_seqlens, initial_state=None):
+    """prefill() with g and beta formed from the raw gate inputs by gate()."""
+    g, beta = gate(a, b, a_log, dt_bias)
+    return prefill(q, k, v, g, beta, cu_seqlens, initial_state)
+
+
+def decode_gated(q, k, v, a, b, a_log, dt_bias, state):
+    """decode() with g and beta formed from the raw gate inputs by gate()."""
+    g, beta = gate(a, b, a_log, dt_bias)
+    return decode(q, k, v, g, beta, state)

@@ -134,6 +134,37 @@ int gdn_ref_decode(const double *q, const double *k, const double *v,
   return 0;
 }
 
+/*
+ * Gate activation (paper, Section 3.2, the first two display lines of the
+ * one-pass form): the paper's multiplicative gate is
+ * exp(-exp(A_log) * softplus(a + b_dt)) and beta = sigma(b). The oracle's
+ * recurrence takes the LOG of that gate, so per token t and value head h
+ *
+ *     g[t, h]    = -exp(A_log[h]) * softplus(a[t, h] + dt_bias[h])
+ *     beta[t, h] = 1 / (1 + exp(-b[t, h]))
+ *
+ * with softplus(x) = log(1 + exp(x)), evaluated as x + log1p(exp(-x)) for
+ * x > 0 so that exp never overflows. a, b, g, beta: [T, HV]; A_log, dt_bias:
+ * [HV].
+ */
+static double ref_softplus(double x) {
+  return x > 0.0 ? x + log1p(exp(-x)) : log1p(exp(x));
+}
+
+int gdn_ref_gate(const double *a, const double *b, const double *A_log,
+                 const double *dt_bias, double *g, double *beta,
+                 int64_t n_tokens, int32_t hv) {
+  if (n_tokens < 0 || hv <= 0) return -1;
+  for (int64_t t = 0; t < n_tokens; ++t) {
+    for (int32_t h = 0; h < hv; ++h) {
+      const size_t i = (size_t)t * hv + h;
+      g[i] = -exp(A_log[h]) * ref_softplus(a[i] + dt_bias[h]);
+      beta[i] = 1.0 / (1.0 + exp(-b[i]));
+    }
+  }
+  return 0;
+}
+
 int gdn_ref_num_threads(void) {
 #ifdef _OPENMP
   return omp_get_max_threads();

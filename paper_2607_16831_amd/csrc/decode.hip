@@ -14,21 +14,30 @@
 // values is covered by D/4 lanes with one 16-byte access each, so a wavefront
 // touches 64*4/D rows per pass and makes PASSES passes; all PASSES loads are
 // issued before any reduction so every lane keeps PASSES x 16 bytes in flight.
+// PASSES is chosen per call (the paper's decode lesson, Section 5.4: decode is
+// a launch-shape problem per batch regime): 4 when that grid still gives every
+// CU two work-groups, else 2, which doubles the work-groups of a small batch
+// (measured on MI355X, d = 128, 32 value heads: B = 1 takes 3.4 us with 2
+// passes against 3.8 us with 4; from B = 8 on, 4 passes are as fast or faster).
 // State traffic uses non-temporal loads and stores: each byte is touched once.
+//
+// With raw gate inputs (a_log != NULL) the gate and beta are formed here from
+// a, b, A_log and dt_bias (Section 3.2) instead of being read.
 #include "gdn_device.h"
 #include "gdn_launch.h"
 
 namespace gdn {
 
-template <int D, typename TIn>
+template <int D, int PASSES, typename TIn>
 __global__ __launch_bounds__(256) void decode_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k,
     const TIn *__restrict__ v, const float *__restrict__ g,
-    const float *__restrict__ beta, float *__restrict__ state,
+    const float *__restrict__ beta, const float *__restrict__ ga,
+    const float *__restrict__ gb, const float *__restrict__ a_log,
+    const float *__restrict__ dt_bias, float *__restrict__ state,
     TIn *__restrict__ o, int64_t total_rows, int hqk, int hv, int group) {
   constexpr int LPR = D / 4;            // lanes per state row
   constexpr int RPP = kWave / LPR;      // rows per pass
-  constexpr int PASSES = 4;
   constexpr int ROWS_PER_WAVE = RPP * PASSES;
   static_assert(D % ROWS_PER_WAVE == 0, "a wavefront must stay in one head");
 
@@ -57,8 +66,14 @@ __global__ __launch_bounds__(256) void decode_kernel(
 #pragma unroll
   for (int p = 0; p < PASSES; ++p)
     vv[p] = Elem<TIn>::load1(v + pair * D + r0 + p * RPP + sub);
-  const float alpha = __expf(g[pair]);
-  const float bt = beta[pair];
+  float alpha, bt;
+  if (a_log != nullptr) {  // uniform over the launch
+    alpha = __expf(gate_log_decay(ga[pair], a_log[h], dt_bias[h]));
+    bt = gate_beta(gb[pair]);
+  } else {
+    alpha = __expf(g[pair]);
+    bt = beta[pair];
+  }
 
   float qk = qq[0] * kk[0] + qq[1] * kk[1] + qq[2] * kk[2] + qq[3] * kk[3];
   qk = group_sum<LPR>(qk);
@@ -79,18 +94,39 @@ __global__ __launch_bounds__(256) void decode_kernel(
   }
 }
 
-template <int D, typename TIn>
-static hipError_t launch_decode_t(const DecodeArgs &a) {
-  constexpr int ROWS_PER_WAVE = (kWave / (D / 4)) * 4;
-  const int64_t total_rows = (int64_t)a.batch * a.hv * D;
+template <int D, int PASSES, typename TIn>
+static hipError_t launch_decode_p(const DecodeArgs &a, int64_t total_rows) {
+  constexpr int ROWS_PER_WAVE = (kWave / (D / 4)) * PASSES;
   const int64_t rows_per_block = ROWS_PER_WAVE * 4;
   const int64_t blocks = (total_rows + rows_per_block - 1) / rows_per_block;
-  if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((decode_kernel<D, TIn>), dim3((unsigned)blocks), dim3(256),
+  hipLaunchKernelGGL((decode_kernel<D, PASSES, TIn>), dim3((unsigned)blocks), dim3(256),
                      0, a.stream, (const TIn *)a.q, (const TIn *)a.k,
-                     (const TIn *)a.v, a.g, a.beta, a.state, (TIn *)a.o,
-                     total_rows, a.hqk, a.hv, a.hv / a.hqk);
+                     (const TIn *)a.v, a.g, a.beta, a.gate.a, a.gate.b, a.gate.a_log,
+                     a.gate.dt_bias, a.state, (TIn *)a.o, total_rows, a.hqk, a.hv,
+                     a.hv / a.hqk);
   return hipGetLastError();
+}
+
+// Compute units of the current device, read once per process.
+static int device_cus() {
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    return n;
+  }();
+  return cus;
+}
+
+template <int D, typename TIn>
+static hipError_t launch_decode_t(const DecodeArgs &a) {
+  const int64_t total_rows = (int64_t)a.batch * a.hv * D;
+  if (total_rows == 0) return hipSuccess;
+  const int64_t blocks4 = (total_rows + (kWave / (D / 4)) * 16 - 1) / ((kWave / (D / 4)) * 16);
+  if (blocks4 < 2 * (int64_t)device_cus()) return launch_decode_p<D, 2, TIn>(a, total_rows);
+  return launch_decode_p<D, 4, TIn>(a, total_rows);
 }
 
 hipError_t launch_decode(const DecodeArgs &a) {

@@ -150,6 +150,18 @@ struct BufElem<float> {
   }
 };
 
+// ---------------------------------------------------------------- gates
+// Gate activation of the raw inputs (paper, Section 3.2): the log-decay
+// g = -exp(A_log) softplus(a + dt_bias) and beta = sigmoid(b). softplus is
+// evaluated as max(x, 0) + log(1 + exp(-|x|)), which cannot overflow.
+__device__ __forceinline__ float softplus_f32(float x) {
+  return fmaxf(x, 0.f) + log1pf(__expf(-fabsf(x)));
+}
+__device__ __forceinline__ float gate_log_decay(float a, float a_log, float dt_bias) {
+  return -__expf(a_log) * softplus_f32(a + dt_bias);
+}
+__device__ __forceinline__ float gate_beta(float b) { return 1.f / (1.f + __expf(-b)); }
+
 // ---------------------------------------------------------------- reductions
 // Sum over aligned groups of `W` consecutive lanes (W a power of two <= 64).
 template <int W>

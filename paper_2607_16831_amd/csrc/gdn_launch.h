@@ -9,9 +9,16 @@
 
 namespace gdn {
 
+// Raw gate inputs of the *_gated entry points; all NULL when g and beta are
+// passed directly.
+struct GateArgs {
+  const float *a = nullptr, *b = nullptr, *a_log = nullptr, *dt_bias = nullptr;
+};
+
 struct DecodeArgs {
   const void *q, *k, *v;
   const float *g, *beta;
+  GateArgs gate;
   float *state;
   void *o;
   int batch, hqk, hv, d;
@@ -22,6 +29,7 @@ struct DecodeArgs {
 struct PrefillArgs {
   const void *q, *k, *v;
   const float *g, *beta;
+  GateArgs gate;
   const int32_t *cu_seqlens;
   const float *initial_state;
   void *o;

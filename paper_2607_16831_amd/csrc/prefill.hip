@@ -130,7 +130,7 @@ __device__ __forceinline__ int gram_row(int p, int r) {
 template <int D, int C, typename TIn>
 __global__ __launch_bounds__(256) void chunk_local_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k,
-    const float *__restrict__ g, const float *__restrict__ beta,
+    const float *__restrict__ g, const float *__restrict__ beta, GateArgs gate,
     const int32_t *__restrict__ cu, int n_seqs, int hqk, int hv, int group,
     int n_pairs, float *__restrict__ dec_ws, uint16_t *__restrict__ tfrag,
     uint16_t *__restrict__ pfrag, uint16_t *__restrict__ qfrag,
@@ -190,10 +190,23 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   const uint32_t rowb = (uint32_t)(nvalid * hqk * D * sizeof(TIn));
   const rsrc_t rk = make_rsrc(k + (t0 * hqk + hk) * D, rowb);
   const rsrc_t rq = make_rsrc(q + (t0 * hqk + hk) * D, rowb);
-  const rsrc_t rg = make_rsrc(g + t0 * hv, (uint32_t)(nvalid * hv * 4));
-  const rsrc_t rb = make_rsrc(beta + t0 * hv, (uint32_t)(nvalid * hv * 4));
-  const float gl = buf_load_f32(rg, (uint32_t)(lane * hv + h) * 4u);
-  const float bta = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
+  // g and beta of token `lane` (0 past the end), read or formed from the raw
+  // gate inputs
+  float gl, bta;
+  if (gate.a_log != nullptr) {  // uniform over the launch
+    const rsrc_t ra = make_rsrc(gate.a + t0 * hv, (uint32_t)(nvalid * hv * 4));
+    const rsrc_t rb = make_rsrc(gate.b + t0 * hv, (uint32_t)(nvalid * hv * 4));
+    const float ga = buf_load_f32(ra, (uint32_t)(lane * hv + h) * 4u);
+    const float gb = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
+    const bool in = lane < nvalid;
+    gl = in ? gate_log_decay(ga, gate.a_log[h], gate.dt_bias[h]) : 0.f;
+    bta = in ? gate_beta(gb) : 0.f;
+  } else {
+    const rsrc_t rg = make_rsrc(g + t0 * hv, (uint32_t)(nvalid * hv * 4));
+    const rsrc_t rb = make_rsrc(beta + t0 * hv, (uint32_t)(nvalid * hv * 4));
+    gl = buf_load_f32(rg, (uint32_t)(lane * hv + h) * 4u);
+    bta = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
+  }
   if constexpr (sizeof(TIn) == 2) {
     // Buffer-to-LDS copies: lane i of a copy fills bytes [16 i, 16 i + 16) of
     // its 1 KB piece, so the source offset picks the global 16-byte piece that
@@ -997,7 +1010,7 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
     const int64_t pairs = nc * a.hqk;
     const int64_t lblocks = ((pairs + 7) / 8) * 8 * group;
     hipLaunchKernelGGL((chunk_local_kernel<D, C, TIn>), dim3((unsigned)lblocks), dim3(256), 0,
-                       a.stream, (const TIn *)a.q, (const TIn *)a.k, a.g, a.beta,
+                       a.stream, (const TIn *)a.q, (const TIn *)a.k, a.g, a.beta, a.gate,
                        a.cu_seqlens, a.n_seqs, a.hqk, a.hv, group, (int)pairs, dec, tf, pf,
                        qf, kc);
     const hipError_t e = hipGetLastError();

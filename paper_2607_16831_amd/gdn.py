@@ -20,7 +20,7 @@ GDN_OK, GDN_ERR_INVALID_ARG, GDN_ERR_UNSUPPORTED, GDN_ERR_WORKSPACE, GDN_ERR_HIP
 GDN_BF16, GDN_F32 = 0, 1
 
 EXPORTS = ("gdn_status_string", "gdn_version", "gdn_prefill_workspace_size",
-           "gdn_prefill", "gdn_decode")
+           "gdn_prefill", "gdn_decode", "gdn_prefill_gated", "gdn_decode_gated")
 
 _lib = None
 
@@ -54,6 +54,13 @@ def lib() -> ctypes.CDLL:
         L.gdn_decode.argtypes = [vp, vp, vp, fp, fp, fp, vp, i32, i32, i32, i32,
                                  i32, ctypes.c_int, vp]
         L.gdn_decode.restype = ctypes.c_int
+        L.gdn_prefill_gated.argtypes = [vp, vp, vp, fp, fp, fp, fp, ip, fp, vp, fp, i32,
+                                        i64, i32, i32, i32, i32, i32, ctypes.c_int, vp, sz,
+                                        vp]
+        L.gdn_prefill_gated.restype = ctypes.c_int
+        L.gdn_decode_gated.argtypes = [vp, vp, vp, fp, fp, fp, fp, fp, vp, i32, i32, i32,
+                                       i32, i32, ctypes.c_int, vp]
+        L.gdn_decode_gated.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -114,6 +121,23 @@ def decode_raw(q, k, v, g, beta, state, o, batch, hqk, hv, dk, dv, dtype,
                                 dv, dtype, stream))
 
 
+def prefill_gated_raw(q, k, v, a, b, a_log, dt_bias, cu_seqlens, initial_state, o,
+                      final_state, n_seqs, n_tokens, hqk, hv, dk, dv, chunk, dtype,
+                      workspace, workspace_bytes, stream) -> int:
+    """Direct call of gdn_prefill_gated with integer pointers; returns the status."""
+    return int(lib().gdn_prefill_gated(q, k, v, a, b, a_log, dt_bias, cu_seqlens,
+                                       initial_state, o, final_state, n_seqs, n_tokens,
+                                       hqk, hv, dk, dv, chunk, dtype, workspace,
+                                       workspace_bytes, stream))
+
+
+def decode_gated_raw(q, k, v, a, b, a_log, dt_bias, state, o, batch, hqk, hv, dk, dv,
+                     dtype, stream) -> int:
+    """Direct call of gdn_decode_gated with integer pointers; returns the status."""
+    return int(lib().gdn_decode_gated(q, k, v, a, b, a_log, dt_bias, state, o, batch,
+                                      hqk, hv, dk, dv, dtype, stream))
+
+
 def alloc_workspace(n_seqs, n_tokens, hqk, hv, d, chunk, device) -> torch.Tensor:
     nbytes = prefill_workspace_size(n_seqs, n_tokens, hqk, hv, d, d, chunk)
     if nbytes == 0:
@@ -171,4 +195,70 @@ def decode(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor,
                     _ptr(o), B, hqk, hv, dk, dv, _dtype_code(q), _stream(stream))
     if st != GDN_OK:
         raise GdnError("gdn_decode", st)
+    return o
+
+
+def _check_gate(a, b, a_log, dt_bias, rows, hv):
+    for name, t in (("a", a), ("b", b), ("A_log", a_log), ("dt_bias", dt_bias)):
+        if t.dtype != torch.float32:
+            raise TypeError("%s must be float32" % name)
+    if tuple(a.shape) != (rows, hv) or tuple(b.shape) != (rows, hv):
+        raise ValueError("a and b must be [%d, %d]" % (rows, hv))
+    if tuple(a_log.shape) != (hv,) or tuple(dt_bias.shape) != (hv,):
+        raise ValueError("A_log and dt_bias must be [%d]" % hv)
+
+
+def prefill_gated(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, a: torch.Tensor,
+                  b: torch.Tensor, a_log: torch.Tensor, dt_bias: torch.Tensor,
+                  cu_seqlens: torch.Tensor, initial_state: Optional[torch.Tensor] = None,
+                  chunk: int = 64, o: Optional[torch.Tensor] = None,
+                  final_state: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None,
+                  stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Chunked prefill from the raw gate inputs a, b [T, HV], A_log, dt_bias [HV]."""
+    T, hqk, dk = q.shape
+    hv, dv = v.shape[1], v.shape[2]
+    N = cu_seqlens.shape[0] - 1
+    _check_gate(a, b, a_log, dt_bias, T, hv)
+    if o is None:
+        o = torch.empty((T, hv, dv), dtype=q.dtype, device=q.device)
+    if final_state is None:
+        final_state = torch.empty((N, hv, dv, dk), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = alloc_workspace(N, T, hqk, hv, dk, chunk, q.device)
+    _check_dev(q, k, v, a, b, a_log, dt_bias, cu_seqlens, initial_state, o, final_state,
+               workspace)
+    if cu_seqlens.dtype != torch.int32:
+        raise TypeError("cu_seqlens must be int32")
+    if k.dtype != q.dtype or v.dtype != q.dtype or o.dtype != q.dtype:
+        raise TypeError("q, k, v and o must share one dtype")
+    st = prefill_gated_raw(_ptr(q), _ptr(k), _ptr(v), _ptr(a), _ptr(b), _ptr(a_log),
+                           _ptr(dt_bias), _ptr(cu_seqlens), _ptr(initial_state), _ptr(o),
+                           _ptr(final_state), N, T, hqk, hv, dk, dv, chunk, _dtype_code(q),
+                           _ptr(workspace), workspace.numel(), _stream(stream))
+    if st != GDN_OK:
+        raise GdnError("gdn_prefill_gated", st)
+    return o, final_state
+
+
+def decode_gated(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, a: torch.Tensor,
+                 b: torch.Tensor, a_log: torch.Tensor, dt_bias: torch.Tensor,
+                 state: torch.Tensor, o: Optional[torch.Tensor] = None,
+                 stream=None) -> torch.Tensor:
+    """One decode step from the raw gate inputs; advances ``state`` in place."""
+    B, hqk, dk = q.shape
+    hv, dv = v.shape[1], v.shape[2]
+    _check_gate(a, b, a_log, dt_bias, B, hv)
+    if o is None:
+        o = torch.empty((B, hv, dv), dtype=q.dtype, device=q.device)
+    _check_dev(q, k, v, a, b, a_log, dt_bias, state, o)
+    if state.dtype != torch.float32:
+        raise TypeError("state must be float32")
+    if k.dtype != q.dtype or v.dtype != q.dtype or o.dtype != q.dtype:
+        raise TypeError("q, k, v and o must share one dtype")
+    st = decode_gated_raw(_ptr(q), _ptr(k), _ptr(v), _ptr(a), _ptr(b), _ptr(a_log),
+                          _ptr(dt_bias), _ptr(state), _ptr(o), B, hqk, hv, dk, dv,
+                          _dtype_code(q), _stream(stream))
+    if st != GDN_OK:
+        raise GdnError("gdn_decode_gated", st)
     return o

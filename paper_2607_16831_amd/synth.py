@@ -15,12 +15,18 @@ contest's 54 decode and 100 prefill workloads):
   decay (alpha ~ 0.98) that keeps the state carry visible in the outputs.
 * beta = sigmoid(N(0, 1)).
 * initial states ~ N(0, 0.1^2) where present.
+* raw gate inputs (workloads with raw_gate): a, b ~ N(0, 1) per (token, head),
+  A_log = log(A) with A ~ U(1, 16) per head, and dt_bias the inverse softplus
+  of dt = exp(U(log 0.001, log 0.1)) per head -- the usual initialisation of
+  these parameters in gated linear-attention layers; g and beta are then
+  formed from them in fp32 (the kernels form their own).
 * q, k, v are produced in fp32 and rounded to bf16 (round to nearest even)
   when the workload is bf16; g, beta and states stay fp32.
 
 One seeded torch CPU generator per workload (deterministic for a given seed
 and torch build); draw order: sequence lengths, q, k, v, g noise, beta noise,
-initial state. Arithmetic on the draws is fp32.
+initial state, then (raw_gate only) a, b, A, dt. Arithmetic on the draws is
+fp32.
 """
 from __future__ import annotations
 
@@ -48,6 +54,7 @@ class Workload:
     g_zero: bool = False            # alpha = 1 exactly
     g_scale: float = 1.0            # multiplies g (stress: very strong decay)
     state_std: float = 0.0          # 0 -> no initial state
+    raw_gate: bool = False          # also draw a, b, A_log, dt_bias
     seed: int = 1000
 
     def replace(self, **kw) -> "Workload":
@@ -102,7 +109,9 @@ def make(w: Workload, seed: Optional[int] = None) -> dict:
 
     Returns a dict with q, k, v (bf16 or f32), g, beta (f32), cu_seqlens
     (int32), initial_state (f32 or None; for decode the state that is
-    advanced in place) and the workload itself under "w".
+    advanced in place) and the workload itself under "w". With w.raw_gate it
+    also holds a, b [T, HV] and A_log, dt_bias [HV] (f32), and g, beta are
+    formed from them.
     """
     gen = torch.Generator().manual_seed(w.seed if seed is None else seed)
     lens = seq_lengths(w, gen)
@@ -125,6 +134,19 @@ def make(w: Workload, seed: Optional[int] = None) -> dict:
         s0 = torch.zeros((w.n_seqs, w.hv, d, d))
     cu = np.zeros(w.n_seqs + 1, dtype=np.int32)
     cu[1:] = np.cumsum(lens)
-    return dict(w=w, q=_cast(q, w.dtype), k=_cast(k, w.dtype), v=_cast(v, w.dtype),
-                g=g.float().contiguous(), beta=beta.float().contiguous(),
-                initial_state=s0, cu_seqlens=torch.from_numpy(cu))
+    out = dict(w=w, q=_cast(q, w.dtype), k=_cast(k, w.dtype), v=_cast(v, w.dtype),
+               initial_state=s0, cu_seqlens=torch.from_numpy(cu))
+    if w.raw_gate:
+        a = torch.randn((T, w.hv), generator=gen)
+        b = torch.randn((T, w.hv), generator=gen)
+        A = 1.0 + 15.0 * torch.rand((w.hv,), generator=gen)
+        dt = torch.exp(np.log(1e-3) + (np.log(1e-1) - np.log(1e-3)) *
+                       torch.rand((w.hv,), generator=gen))
+        dt_bias = dt + torch.log(-torch.expm1(-dt))  # softplus(dt_bias) = dt
+        a_log = torch.log(A)
+        g = -torch.exp(a_log) * torch.nn.functional.softplus(a + dt_bias)
+        beta = torch.sigmoid(b)
+        out.update(a=a.contiguous(), b=b.contiguous(), A_log=a_log.contiguous(),
+                   dt_bias=dt_bias.contiguous())
+    out.update(g=g.float().contiguous(), beta=beta.float().contiguous())
+    return out

@@ -104,6 +104,42 @@ def test_decode_validation():
     assert _decode(batch=0, q=None, state=None) == E.GDN_OK
 
 
+def _prefill_gated(**kw):
+    args = dict(q=FAKE, k=FAKE, v=FAKE, a=FAKE, b=FAKE, a_log=FAKE, dt_bias=FAKE,
+                cu_seqlens=FAKE, initial_state=None, o=FAKE, final_state=FAKE, n_seqs=1,
+                n_tokens=64, hqk=1, hv=1, dk=32, dv=32, chunk=16, dtype=gdn.GDN_F32,
+                workspace=FAKE, workspace_bytes=0, stream=None)
+    args.update(kw)
+    return gdn.prefill_gated_raw(**args)
+
+
+def _decode_gated(**kw):
+    args = dict(q=FAKE, k=FAKE, v=FAKE, a=FAKE, b=FAKE, a_log=FAKE, dt_bias=FAKE,
+                state=FAKE, o=FAKE, batch=4, hqk=2, hv=4, dk=64, dv=64,
+                dtype=gdn.GDN_BF16, stream=None)
+    args.update(kw)
+    return gdn.decode_gated_raw(**args)
+
+
+def test_gated_validation():
+    E = gdn
+    for name in ("a", "b", "a_log", "dt_bias"):
+        assert _prefill_gated(**{name: None}) == E.GDN_ERR_INVALID_ARG, name
+        assert _decode_gated(**{name: None}) == E.GDN_ERR_INVALID_ARG, name
+    assert _prefill_gated(dk=96, dv=96) == E.GDN_ERR_UNSUPPORTED
+    assert _prefill_gated(hqk=2, hv=3) == E.GDN_ERR_INVALID_ARG
+    # the gated call sizes its workspace like the plain one
+    need = gdn.prefill_workspace_size(1, 64, 1, 1, 32, 32, 16)
+    assert _prefill_gated(workspace_bytes=need - 1) == E.GDN_ERR_WORKSPACE
+    assert _prefill_gated(n_seqs=0, n_tokens=0, q=None, a=None, b=None, a_log=None,
+                          dt_bias=None, cu_seqlens=None) == E.GDN_OK
+    assert _decode_gated(batch=0, q=None, a=None, state=None) == E.GDN_OK
+    assert _decode_gated(dtype=5) == E.GDN_ERR_UNSUPPORTED
+    # the plain entry points still need g and beta
+    assert _prefill(g=None) == E.GDN_ERR_INVALID_ARG
+    assert _decode(beta=None) == E.GDN_ERR_INVALID_ARG
+
+
 def test_binding_refuses_host_tensors():
     import torch
     x = torch.zeros(4, 1, 32)

@@ -88,6 +88,23 @@ def test_decode_shapes(d, dtype, hqk, hv):
     assert eo <= (O_BAR if dtype == "bf16" else 1e-5) and es <= 1e-5
 
 
+@pytest.mark.parametrize("B", [1, 2, 8, 16, 48])
+def test_decode_small_batches(B):
+    """Both launch shapes of the decode kernel (2 passes below two work-groups
+    per CU, 4 above) at the benchmark's heads and head size."""
+    dev = require_gpu()
+    x = synth.make(synth.DECODE_B64.replace(n_seqs=B, seed=40 + B))
+    d = to_dev(x, dev)
+    state = d["initial_state"].clone()
+    o = gdn.decode(d["q"], d["k"], d["v"], d["g"], d["beta"], state)
+    torch.cuda.synchronize()
+    o_ref, s_ref = oracle.decode(x["q"], x["k"], x["v"], x["g"], x["beta"],
+                                 x["initial_state"])
+    eo, es = rel_l2(o.cpu(), o_ref), rel_l2(state.cpu(), s_ref)
+    _log("decode_B%d" % B, o=eo, state=es)
+    assert eo <= O_BAR and es <= 1e-5
+
+
 def test_decode_repeated_steps_match_prefill():
     """Eight decode steps on the GPU == one 8-token prefill (oracle-checked)."""
     dev = require_gpu()

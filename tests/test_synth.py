@@ -48,3 +48,18 @@ def test_decode_workload():
     assert x["q"].shape == (64, 2, 16) and x["v"].shape == (64, 4, 16)
     assert x["g"].shape == (64, 4)
     assert x["initial_state"].shape == (64, 4, 16, 16)
+
+
+def test_raw_gate_draws_leave_other_inputs_alone():
+    w = synth.PREFILL_VARLEN.replace(hqk=1, hv=3, d=8, n_seqs=3)
+    x, y = synth.make(w), synth.make(w.replace(raw_gate=True))
+    for key in ("q", "k", "v", "cu_seqlens", "initial_state"):
+        assert torch.equal(x[key], y[key]), key
+    T = y["q"].shape[0]
+    assert y["a"].shape == (T, 3) and y["b"].shape == (T, 3)
+    assert y["A_log"].shape == (3,) and y["dt_bias"].shape == (3,)
+    A = y["A_log"].exp()
+    assert (A >= 1).all() and (A <= 16).all()
+    dt = torch.nn.functional.softplus(y["dt_bias"].double())
+    assert (dt >= 0.999e-3).all() and (dt <= 0.1001).all()
+    assert (y["g"] < 0).all() and (y["beta"] > 0).all() and (y["beta"] < 1).all()
