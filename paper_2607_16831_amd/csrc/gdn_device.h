@@ -118,6 +118,10 @@ __device__ __forceinline__ float4 buf_load_f32x4(rsrc_t r, uint32_t off) {
                      __uint_as_float(x.z), __uint_as_float(x.w));
 }
 
+// Cache-policy operand of the buffer intrinsics: the non-temporal (streaming)
+// bit of gfx940-family targets (the position of SLC on earlier gfx9).
+constexpr int kCachePolicyNT = 2;
+
 // Element access through a buffer resource; offsets are in elements.
 template <typename T>
 struct BufElem;
@@ -133,6 +137,11 @@ struct BufElem<__bf16> {
   static __device__ __forceinline__ void store1(rsrc_t r, uint32_t e, float x) {
     __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_bits(x), r, e * 2u, 0, 0);
   }
+  // Streaming store (non-temporal): written out to memory as the kernel runs
+  // instead of staying dirty in L2 until the kernel ends.
+  static __device__ __forceinline__ void store1_stream(rsrc_t r, uint32_t e, float x) {
+    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_bits(x), r, e * 2u, 0, kCachePolicyNT);
+  }
 };
 
 template <>
@@ -147,6 +156,9 @@ struct BufElem<float> {
   }
   static __device__ __forceinline__ void store1(rsrc_t r, uint32_t e, float x) {
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, e * 4u, 0, 0);
+  }
+  static __device__ __forceinline__ void store1_stream(rsrc_t r, uint32_t e, float x) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, e * 4u, 0, kCachePolicyNT);
   }
 };
 

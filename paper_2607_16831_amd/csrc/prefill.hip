@@ -439,9 +439,17 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
 // order) are loaded straight into its registers one chunk ahead, 1 KB per
 // contiguous load. What several wavefronts share goes through LDS: K (rows
 // for X, columns for the state update), the V tile and the decay factors,
-// copied by the two loader wavefronts with buffer-to-LDS loads into the
-// buffer the compute wavefronts are not reading. The loaders also write back
-// the output tiles, which the compute wavefronts stage in LDS.
+// copied by the two loader wavefronts with buffer-to-LDS loads into a buffer
+// the compute wavefronts are not reading.
+//
+// Per chunk, three phases separated by work-group barriers carry the chain
+// X -> Y -> U -> state; each phase reads from LDS only what the phase before
+// produced (S^T, Y, U). Everything else a phase needs -- K rows and K^T
+// operands, V and the decay factors -- is read into registers a phase or
+// more ahead: waves 0-3 read those of chunk c + 1 right after the state
+// update of chunk c (the reads stay in flight across the barrier), waves
+// 4-7 their K^T operands in phase 1. Outputs go from registers straight to
+// global memory.
 //
 // Global reads go through buffer resources: rows past the end of the
 // sequence read as zero (beta is zero there, so they add exact zeros) and
@@ -455,14 +463,14 @@ struct CarryCfg {
   static constexpr int ESZ = (int)sizeof(TIn);
   static constexpr int KPR = D / 8;              // 16-byte units per bf16 K row
   static constexpr int NKI = C * D / 512;        // 1 KB copies per K chunk
-  static constexpr int VPR = ESZ;                // 16-byte units per token of a V/O tile row
-  static constexpr int VU = C * VPR;             // 16-byte units of the V (or O) tile
+  static constexpr int VPR = ESZ;                // 16-byte units per token of a V tile row
+  static constexpr int VU = C * VPR;             // 16-byte units of the V tile
   static constexpr int NVI = (VU + 63) / 64;     // 1 KB copies per V tile
   static constexpr int NDI = (2 * C + 255) / 256;  // 1 KB copies of the 2C decay factors
   static constexpr int M = NKI + NVI + NDI;      // copies per chunk
   static constexpr int SLOTS = (M + NLW - 1) / NLW;
-  static constexpr int NOU = (VU + 64 * NLW - 1) / (64 * NLW);  // output units per loader lane
-  static constexpr int NB = 3;                   // LDS buffers of the copied inputs
+  static constexpr int NB = 4;                   // LDS buffers of the copied inputs
+  static constexpr int NA = NB - 1;              // chunks issued ahead of the one in use
   static_assert(NT == 640, "launch bounds of the carry kernel");
 };
 
@@ -472,11 +480,9 @@ template <int D, int C, typename TIn>
 struct CarryLds {
   using F = Cfg<D, C>;
   using CC = CarryCfg<D, C, TIn>;
-  // The copied inputs of chunk lc live in buffer lc % NB; the output tile of
-  // chunk lc is staged in Ol[lc & 1].
+  // The copied inputs of chunk lc live in buffer lc % NB.
   uint16_t Kn[CC::NB][F::CP * D];  // K chunk, row-major, swizzled; rows C..CP-1 stay zero
   uint4 Vl[CC::NB][CC::NVI * 64];  // V tile, [token][16 values], input element type
-  uint4 Ol[2][CC::NVI * 64];       // output tile, same layout
   float Dl[CC::NB][CC::NDI * 256];  // exp(gamma_i), then exp(gamma_last - gamma_i)
   uint16_t Sl[16 * F::LDK];     // bf16 copy of the state tile, [value][key]
   uint16_t Yl[16 * F::LDV];     // Y,  [value][token position]
@@ -554,35 +560,12 @@ __device__ __forceinline__ void issue_copy(CarryLds<D, C, TIn> &L, int bb, const
   }
 }
 
-// Output tile of one chunk, staged in LDS as [token][16 values], to global.
-template <int D, int C, typename TIn>
-__device__ __forceinline__ void store_out(const CarryLds<D, C, TIn> &L, int bb, rsrc_t ro,
-                                          const int *op, const uint32_t *ooff) {
-  using CC = CarryCfg<D, C, TIn>;
-#pragma unroll
-  for (int j = 0; j < CC::NOU; ++j) {
-    if (op[j] < CC::VU) {
-      const uint4 x = L.Ol[bb][op[j]];
-      __builtin_amdgcn_raw_buffer_store_b128(
-          (__attribute__((ext_vector_type(4))) unsigned int){x.x, x.y, x.z, x.w}, ro, ooff[j], 0, 0);
-    }
-  }
-}
-
-// Copies loader LW issues per chunk, and output stores it issues per chunk
-// (a store instruction is issued when its first lane is in range).
+// Copies loader LW issues per chunk.
 template <int D, int C, typename TIn, int LW>
 constexpr int loader_copies() {
   using CC = CarryCfg<D, C, TIn>;
   int n = 0;
   for (int i = 0; i < CC::SLOTS; ++i) n += (CC::NLW * i + LW < CC::M) ? 1 : 0;
-  return n;
-}
-template <int D, int C, typename TIn, int LW>
-constexpr int loader_stores() {
-  using CC = CarryCfg<D, C, TIn>;
-  int n = 0;
-  for (int j = 0; j < CC::NOU; ++j) n += (64 * (LW + CC::NLW * j) < CC::VU) ? 1 : 0;
   return n;
 }
 
@@ -593,29 +576,31 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Work-group barrier that lets the youngest N LDS operations of this
+// wavefront stay in flight. LDS operations complete in issue order, so every
+// LDS access issued before those N (a state write, say) is complete and
+// visible to the other wavefronts after the barrier.
+template <int N>
+__device__ __forceinline__ void lds_barrier_keep() {
+  static_assert(N >= 0 && N <= 15, "LDS counter range");
+  asm volatile("s_waitcnt lgkmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
 // Loader wavefront LW (a template parameter, so that the kind of each of its
-// copies is known when compiling). The copies of chunk lc + 2 are issued
-// while the compute wavefronts work on chunk lc, and only those of chunk
-// lc + 1 must have landed by the end of chunk lc; the output stores are never
-// waited for (their data is read out of LDS when they issue).
+// copies is known when compiling). The copies of chunk lc + NA are issued at
+// the start of chunk lc into the buffer chunk lc - 1 used, and chunk lc + 1
+// must have landed before the second barrier of chunk lc: waves 0-3 read it
+// in phase 3.
 template <int D, int C, typename TIn, int LW>
 __device__ __forceinline__ void carry_loader(
     CarryLds<D, C, TIn> &L, int lane, const uint16_t *__restrict__ ksrc, int kstride,
-    bool kcopied, const TIn *__restrict__ v, const float *__restrict__ dec_ws,
-    TIn *__restrict__ o, int nch, int64_t seq_t0, int64_t seq_t1, int64_t c0, int h,
-    int hk, int hqk, int hv, int v0) {
+    bool kcopied, const TIn *__restrict__ v, const float *__restrict__ dec_ws, int nch,
+    int64_t seq_t0, int64_t seq_t1, int64_t c0, int h, int hk, int hqk, int hv, int v0) {
   using CC = CarryCfg<D, C, TIn>;
   constexpr int NS = CC::SLOTS;
   uint32_t off[NS];
 #pragma unroll
   for (int i = 0; i < NS; ++i) off[i] = copy_offset<D, C, TIn>(CC::NLW * i + LW, lane, kstride, hv);
-  int op[CC::NOU];
-  uint32_t ooff[CC::NOU];
-#pragma unroll
-  for (int j = 0; j < CC::NOU; ++j) {
-    op[j] = 64 * (LW + CC::NLW * j) + lane;
-    ooff[j] = (uint32_t)(((op[j] / CC::VPR) * hv * D + (op[j] % CC::VPR) * (16 / CC::ESZ)) * CC::ESZ);
-  }
 
   auto res = [&](int lc) {
     const int64_t t0 = seq_t0 + (int64_t)lc * C;
@@ -629,16 +614,10 @@ __device__ __forceinline__ void carry_loader(
     r.d = make_rsrc(dec_ws + ((c0 + lc) * hv + h) * 2 * C, 2 * C * 4);
     return r;
   };
-  auto out_res = [&](int lc, bool live) {
-    const int64_t t0 = seq_t0 + (int64_t)lc * C;
-    const int nv = live ? (int)min((int64_t)C, seq_t1 - t0) : 0;
-    return make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * CC::ESZ));
-  };
 
   constexpr int NCP = loader_copies<D, C, TIn, LW>();
-  constexpr int NST = loader_stores<D, C, TIn, LW>();
-  constexpr int NA = CC::NB - 1;  // chunks in flight ahead of the one in use
-  auto issue = [&](int lc) {      // chunk lc into buffer lc % NB
+  constexpr int NA = CC::NA;
+  auto issue = [&](int lc) {  // chunk lc into buffer lc % NB
     const CopyRes R = res(lc);
 #pragma unroll
     for (int i = 0; i < NS; ++i) issue_copy<D, C, TIn>(L, lc % CC::NB, R, CC::NLW * i + LW, off[i]);
@@ -653,62 +632,48 @@ __device__ __forceinline__ void carry_loader(
   lds_barrier();
 
   for (int lc = 0; lc < nch; ++lc) {
-    // output of chunk lc - 2 (staged during phase 1 of chunk lc - 1), then
-    // chunk lc + NA into the buffer chunk lc - 1 used
-    store_out<D, C, TIn>(L, lc & 1, out_res(max(lc - 2, 0), lc >= 2), op, ooff);
     if (lc + NA < nch) issue(lc + NA);
     lds_barrier();
-    lds_barrier();
-    // Chunk lc + 1 must have landed before the last barrier of chunk lc. In
-    // the steady state NA - 1 later iterations' stores and copies are still
-    // allowed in flight; near either end everything is waited for.
-    if (lc >= NA - 2 && lc + NA < nch)
-      wait_vm<(NA - 1) * (NST + NCP)>();
+    // Chunk lc + 1 must have landed. While copies are still issued every
+    // chunk, those of the NA - 1 later chunks may stay in flight; near the
+    // end everything is waited for.
+    if (lc + NA < nch)
+      wait_vm<(NA - 1) * NCP>();
     else
       wait_vm<0>();
     lds_barrier();
+    lds_barrier();
   }
-  // outputs of the last two chunks
-  store_out<D, C, TIn>(L, nch & 1, out_res(max(nch - 2, 0), nch >= 2), op, ooff);
-  lds_barrier();
-  store_out<D, C, TIn>(L, (nch - 1) & 1, out_res(nch - 1, true), op, ooff);
 }
 
 // ---------------------------------------------------------------- compute
 // Per chunk c, three phases separated by work-group barriers:
 //   1. waves 0-3: X = K S^T for their token block, Y = V - exp(gamma) X.
 //      waves 4-7: O of chunk c-1 = exp(gamma) Q S^T + P U (their operands
-//      were kept from chunk c-1; U of chunk c-1 is still in LDS).
+//      were kept from chunk c-1; U of chunk c-1 is still in LDS), stored to
+//      global memory; the K^T operands of chunk c.
 //   2. waves 0-3: U = T' Y and exp(gamma_last - gamma) U.
 //      waves 4-7: Q S^T (S is still the state entering chunk c).
 //   3. all eight: S^T <- exp(gamma_last) S^T + K^T (exp(gamma_last - gamma) U)
-//      for their key tile.
+//      for their key tile; waves 0-3 then read chunk c + 1's operands.
 // The chain from one state to the next runs through phases 1-3 on waves 0-3
 // and the update; the output work fills the phases where it would idle.
 template <int D, int C, typename TIn>
-struct StateTile {
-  uint4 kt[Cfg<D, C>::KS];
-  __device__ __forceinline__ void fetch(const CarryLds<D, C, TIn> &L, int b, int wave, int l16,
-                                        int g4) {
+__device__ __forceinline__ void state_update(CarryLds<D, C, TIn> &L, f32x4 &S, const uint4 *kt,
+                                             float glast, int wave, int l16, int g4) {
+  using F = Cfg<D, C>;
+  uint4 bu[F::KS];
 #pragma unroll
-    for (int s = 0; s < Cfg<D, C>::KS; ++s) kt[s] = kt_operand<D>(L.Kn[b], wave, s, l16, g4);
-  }
-  __device__ __forceinline__ void update(CarryLds<D, C, TIn> &L, f32x4 &S, int b, int wave,
-                                         int l16, int g4) {
-    using F = Cfg<D, C>;
-    uint4 bu[F::KS];
+  for (int s = 0; s < F::KS; ++s)
+    bu[s] = *reinterpret_cast<const uint4 *>(&L.Uh[l16 * F::LDV + 32 * s + 8 * g4]);
+  f32x4 acc = S * glast;
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int s = 0; s < F::KS; ++s)
-      bu[s] = *reinterpret_cast<const uint4 *>(&L.Uh[l16 * F::LDV + 32 * s + 8 * g4]);
-    f32x4 acc = S * L.Dl[b][C - 1];
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int s = 0; s < F::KS; ++s) acc = mfma_16x16x32(kt[s], bu[s], acc);
-    S = acc;
-    *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
-        pack4_bf16(acc[0], acc[1], acc[2], acc[3]);
-  }
-};
+  for (int s = 0; s < F::KS; ++s) acc = mfma_16x16x32(kt[s], bu[s], acc);
+  S = acc;
+  *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
+      pack4_bf16(acc[0], acc[1], acc[2], acc[3]);
+}
 
 // Wavefronts 0-3: X, Y and U for token block ib. Each role runs its own loop
 // (with the same barriers) so that every register prefetched for the next
@@ -718,6 +683,7 @@ __device__ __forceinline__ void carry_compute_xu(
     CarryLds<D, C, TIn> &L, f32x4 &S, int wave, int lane, int nch, int64_t c0,
     const uint16_t *__restrict__ tfrag, int h, int hv) {
   using F = Cfg<D, C>;
+  using CC = CarryCfg<D, C, TIn>;
   const int l16 = lane & 15, g4 = lane >> 4;
   const int ib = wave;
   const bool blk = (F::NIB == 4) || (ib < F::NIB);
@@ -732,41 +698,52 @@ __device__ __forceinline__ void carry_compute_xu(
   auto frag_res = [&](int lc) {
     return make_rsrc(tfrag + ((c0 + lc) * hv + h) * F::FRAG, F::FRAG * 2);
   };
-  uint4 fa[F::KS];   // T' rows of block ib, one chunk ahead
+  // operands of the chunk in use, read ahead
+  uint4 fa[F::KS];   // T' rows of block ib (global)
+  uint4 ka[F::DS];   // K rows of block ib (LDS)
+  uint4 kt[F::KS];   // K^T operands of key tile `wave` (LDS)
+  float vv[4], ge[4], he[4], glast = 0.f;
+  auto fetch_lds = [&](int b) {  // V, decay factors, then K^T and K rows of buffer b
+    if (blk) {
+      const TIn *vt = reinterpret_cast<const TIn *>(L.Vl[b]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) vv[e] = Elem<TIn>::load1(&vt[(tb + e) * 16 + l16]);
+      const float4 ge4 = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
+      const float4 he4 = *reinterpret_cast<const float4 *>(&L.Dl[b][C + tb]);
+      ge[0] = ge4.x; ge[1] = ge4.y; ge[2] = ge4.z; ge[3] = ge4.w;
+      he[0] = he4.x; he[1] = he4.y; he[2] = he4.z; he[3] = he4.w;
+    }
+    glast = L.Dl[b][C - 1];
+    if (own) {
+#pragma unroll
+      for (int s = 0; s < F::KS; ++s) kt[s] = kt_operand<D>(L.Kn[b], wave, s, l16, g4);
+    }
+    if (blk) {
+#pragma unroll
+      for (int s = 0; s < F::DS; ++s)
+        ka[s] = *reinterpret_cast<const uint4 *>(&L.Kn[b][kn_index<D>(16 * ib + l16, 32 * s + 8 * g4)]);
+    }
+  };
   {
     const rsrc_t rt = frag_res(0);
 #pragma unroll
     for (int s = 0; s < F::KS; ++s) fa[s] = buf_load_b128(rt, s < nks ? foff + 1024u * s : kOutOfRange);
   }
-  StateTile<D, C, TIn> st;
+  fetch_lds(0);
   for (int lc = 0; lc < nch; ++lc) {
-    const int b = lc % CarryCfg<D, C, TIn>::NB;  // input buffer of chunk lc
     // ---- phase 1: X = K S^T, Y = V - exp(gamma) X (beta is folded into T')
-    float he[4];
     if (blk) {
-      const float4 ge4 = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
-      const float4 he4 = *reinterpret_cast<const float4 *>(&L.Dl[b][C + tb]);
-      he[0] = he4.x; he[1] = he4.y; he[2] = he4.z; he[3] = he4.w;
-      // every operand read of a phase is issued before its first product
-      uint4 bs[F::DS], ka[F::DS];
+      uint4 bs[F::DS];
 #pragma unroll
-      for (int s = 0; s < F::DS; ++s) {
+      for (int s = 0; s < F::DS; ++s)
         bs[s] = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
-        ka[s] = *reinterpret_cast<const uint4 *>(&L.Kn[b][kn_index<D>(16 * ib + l16, 32 * s + 8 * g4)]);
-      }
-      const TIn *vt = reinterpret_cast<const TIn *>(L.Vl[b]);
-      float vv[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) vv[e] = Elem<TIn>::load1(&vt[(tb + e) * 16 + l16]);
       __builtin_amdgcn_sched_barrier(0);
       f32x4 xs = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < F::DS; ++s) xs = mfma_16x16x32(ka[s], bs[s], xs);
-      const float ge[4] = {ge4.x, ge4.y, ge4.z, ge4.w};
-      float y[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) y[e] = vv[e] - ge[e] * xs[e];
-      *reinterpret_cast<uint2 *>(&L.Yl[l16 * F::LDV + ypos]) = pack4_bf16(y[0], y[1], y[2], y[3]);
+      *reinterpret_cast<uint2 *>(&L.Yl[l16 * F::LDV + ypos]) =
+          pack4_bf16(vv[0] - ge[0] * xs[0], vv[1] - ge[1] * xs[1], vv[2] - ge[2] * xs[2],
+                     vv[3] - ge[3] * xs[3]);
     }
     lds_barrier();
     // ---- phase 2: U = T' Y and exp(gamma_last - gamma) U
@@ -788,24 +765,33 @@ __device__ __forceinline__ void carry_compute_xu(
 #pragma unroll
       for (int s = 0; s < F::KS; ++s) fa[s] = buf_load_b128(rt, s < nks ? foff + 1024u * s : kOutOfRange);
     }
-    if (own) st.fetch(L, b, wave, l16, g4);
     lds_barrier();
-    // ---- phase 3
-    if (own) st.update(L, S, b, wave, l16, g4);
-    lds_barrier();
+    // ---- phase 3: state update, then chunk lc + 1's LDS operands, whose
+    // K^T and K reads may stay in flight across the barrier
+    if (own) {
+      state_update<D, C, TIn>(L, S, kt, glast, wave, l16, g4);
+      asm volatile("" ::"v"(S) : "memory");
+    }
+    if (lc + 1 < nch) {
+      fetch_lds((lc + 1) % CC::NB);
+      lds_barrier_keep<((F::NKT == 8) ? 2 * F::KS : 0) + ((F::NIB == 4) ? F::DS : 0)>();
+    } else {
+      lds_barrier();
+    }
   }
-  lds_barrier();  // the output of the last chunk is staged by waves 4-7
 }
 
-// Wavefronts 4-7: Q S^T in phase 2 and, in phase 1 of the next chunk,
-// O = exp(gamma) Q S^T + P U for token block ib (U of that chunk is still in
-// LDS then). The output tile is staged in LDS for the loader wavefronts.
+// Wavefronts 4-7: the K^T operands of the chunk and the output of the
+// previous one in phase 1, Q S^T in phase 2, O = exp(gamma) Q S^T + P U
+// for token block ib (U of that chunk is still in LDS in the next phase 1).
 template <int D, int C, typename TIn>
 __device__ __forceinline__ void carry_compute_o(
     CarryLds<D, C, TIn> &L, f32x4 &S, int wave, int lane, int nch, int64_t c0,
-    const uint16_t *__restrict__ pfrag, const uint16_t *__restrict__ qfrag, int h, int hk,
-    int hqk, int hv) {
+    const uint16_t *__restrict__ pfrag, const uint16_t *__restrict__ qfrag,
+    TIn *__restrict__ o, int64_t seq_t0, int64_t seq_t1, int h, int hk, int hqk, int hv,
+    int v0) {
   using F = Cfg<D, C>;
+  using CC = CarryCfg<D, C, TIn>;
   const int l16 = lane & 15, g4 = lane >> 4;
   const int ib = wave - 4;
   const bool blk = (F::NIB == 4) || (ib < F::NIB);
@@ -821,7 +807,10 @@ __device__ __forceinline__ void carry_compute_o(
   auto q_res = [&](int lc) {
     return make_rsrc(qfrag + ((c0 + lc) * hqk + hk) * (C * D), C * D * 2);
   };
-  auto out = [&](int bb, const uint4 *pa, const f32x4 &qs, const float *gq) {
+  // O of chunk lc from the kept Q S^T, P and the U of that chunk in LDS,
+  // straight to global memory: lane (l16, g4) element e is row tb + e,
+  // column v0 + l16.
+  auto out = [&](const uint4 *pa, const f32x4 &qs, const float *gq, int lc) {
     uint4 bu[F::KS];
 #pragma unroll
     for (int s = 0; s < F::KS; ++s)
@@ -830,12 +819,16 @@ __device__ __forceinline__ void carry_compute_o(
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < F::KS; ++s) acc = mfma_16x16x32(pa[s], bu[s], acc);
-    TIn *ot = reinterpret_cast<TIn *>(L.Ol[bb]);
+    const int64_t t0 = seq_t0 + (int64_t)lc * C;
+    const int nv = (int)min((int64_t)C, seq_t1 - t0);
+    const rsrc_t ro = make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * CC::ESZ));
 #pragma unroll
-    for (int e = 0; e < 4; ++e) Elem<TIn>::store1(&ot[(tb + e) * 16 + l16], gq[e] * qs[e] + acc[e]);
+    for (int e = 0; e < 4; ++e)
+      BufElem<TIn>::store1_stream(ro, (uint32_t)((tb + e) * hv * D + l16), gq[e] * qs[e] + acc[e]);
   };
   uint4 qf[F::DS];   // Q rows of block ib, one chunk ahead
   uint4 pa[F::KS];   // P rows of block ib of the previous chunk
+  uint4 kt[F::KS];   // K^T operands of key tile `wave`
   f32x4 qs = f32x4{0.f, 0.f, 0.f, 0.f};
   float gq[4] = {0.f, 0.f, 0.f, 0.f};
   {
@@ -845,19 +838,26 @@ __device__ __forceinline__ void carry_compute_o(
 #pragma unroll
     for (int s = 0; s < F::KS; ++s) pa[s] = make_uint4(0, 0, 0, 0);
   }
-  StateTile<D, C, TIn> st;
   for (int lc = 0; lc < nch; ++lc) {
-    const int b = lc % CarryCfg<D, C, TIn>::NB;  // input buffer of chunk lc
-    // ---- phase 1: output of chunk lc - 1 (for lc = 0 a zero tile into a
-    // buffer nothing stores), then P of this chunk
+    const int b = lc % CC::NB;  // input buffer of chunk lc
+    // ---- phase 1: output of chunk lc - 1, then P of this chunk and the K^T
+    // operands of the state update
     if (blk) {
-      out((lc & 1) ^ 1, pa, qs, gq);
+      if (lc > 0) out(pa, qs, gq, lc - 1);
       __builtin_amdgcn_sched_barrier(0);
       const rsrc_t rp = p_res(lc);
 #pragma unroll
       for (int s = 0; s < F::KS; ++s) pa[s] = buf_load_b128(rp, s < nks ? foff + 1024u * s : kOutOfRange);
     }
-    lds_barrier();
+    if (own) {
+#pragma unroll
+      for (int s = 0; s < F::KS; ++s) kt[s] = kt_operand<D>(L.Kn[b], wave, s, l16, g4);
+      // these waves write nothing to LDS in phase 1: the K^T reads may stay
+      // in flight across the barrier
+      lds_barrier_keep<((F::NKT == 8) ? 2 * F::KS : 0)>();
+    } else {
+      lds_barrier();
+    }
     // ---- phase 2: Q S^T (S is still the state entering chunk lc)
     if (blk) {
       uint4 bs[F::DS];
@@ -877,14 +877,12 @@ __device__ __forceinline__ void carry_compute_o(
 #pragma unroll
       for (int s = 0; s < F::DS; ++s) qf[s] = buf_load_b128(rq, qoff + 1024u * s);
     }
-    if (own) st.fetch(L, b, wave, l16, g4);
     lds_barrier();
     // ---- phase 3
-    if (own) st.update(L, S, b, wave, l16, g4);
+    if (own) state_update<D, C, TIn>(L, S, kt, L.Dl[b][C - 1], wave, l16, g4);
     lds_barrier();
   }
-  if (blk) out((nch - 1) & 1, pa, qs, gq);   // output of the last chunk
-  lds_barrier();
+  if (blk) out(pa, qs, gq, nch - 1);  // output of the last chunk
 }
 
 template <int D, int C, typename TIn>
@@ -950,7 +948,8 @@ __global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
       if (wave < 4)
         carry_compute_xu<D, C, TIn>(L, S, wave, lane, nch, c0, tfrag, h, hv);
       else
-        carry_compute_o<D, C, TIn>(L, S, wave, lane, nch, c0, pfrag, qfrag, h, hk, hqk, hv);
+        carry_compute_o<D, C, TIn>(L, S, wave, lane, nch, c0, pfrag, qfrag, o, seq_t0, seq_t1,
+                                   h, hk, hqk, hv, v0);
     } else {
       // bf16 K is copied straight from the input; f32 K from its bf16 copy.
       const bool kcopied = sizeof(TIn) != 2;
@@ -958,17 +957,16 @@ __global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
       const int kstride = kcopied ? D : hqk * D;
       static_assert(CC::NLW == 2, "loader dispatch below");
       if (wave == CC::NCW)
-        carry_loader<D, C, TIn, 0>(L, lane, ksrc, kstride, kcopied, v, dec_ws, o, nch, seq_t0,
+        carry_loader<D, C, TIn, 0>(L, lane, ksrc, kstride, kcopied, v, dec_ws, nch, seq_t0,
                                    seq_t1, c0, h, hk, hqk, hv, v0);
       else
-        carry_loader<D, C, TIn, 1>(L, lane, ksrc, kstride, kcopied, v, dec_ws, o, nch, seq_t0,
+        carry_loader<D, C, TIn, 1>(L, lane, ksrc, kstride, kcopied, v, dec_ws, nch, seq_t0,
                                    seq_t1, c0, h, hk, hqk, hv, v0);
     }
   }
 
   if (own)
-    *reinterpret_cast<float4 *>(sT + ((int64_t)pair * D + v0 + l16) * D + 16 * wave + 4 * g4) =
-        make_float4(S[0], S[1], S[2], S[3]);
+    store_stream(sT + ((int64_t)pair * D + v0 + l16) * D + 16 * wave + 4 * g4, S);
 }
 
 // ============================================================ host side
