@@ -18,6 +18,10 @@ fixed algorithmic counts:
                   + 4 (N + 1)
   decode bytes  = 2 B HV d^2 4 + B (2 HQK + 2 HV) d 2 + 8 B HV
 `traffic` is the counter-measured byte count per launch (see MEASURED_TRAFFIC).
+
+Alongside: `decode_latency_us` (one decode step per batch size, graph-replayed)
+and `prefill_dispatch` (short-sequence batches: the library's chunk choice
+against the fixed 64-token chunk).
 """
 import argparse
 import glob
@@ -80,6 +84,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-decode-sweep", action="store_true",
                     help="skip the small-batch decode latency sweep")
+    ap.add_argument("--no-dispatch-sweep", action="store_true",
+                    help="skip the prefill shape-dispatch comparison over short-sequence batches")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="before warm-up, run a read-once/write-once kernel over MB "
                          "megabytes (three times), whose memory counters calibrate "
@@ -231,6 +237,41 @@ def main():
             lat[str(B)] = round(e0.elapsed_time(e1) * 1e3 / (R * KG), 2)
             del graph
         out["decode_latency_us"] = lat
+
+    # ------------------------------------------------- prefill shape dispatch
+    # Batches of N equal-length sequences (same heads, d and dtype as the
+    # main workload, no initial state): time per call with the library's own
+    # choice (chunk = 0) against the fixed 64-token chunk, 20 calls between
+    # events after 3 warm-up calls, one input set per shape.
+    if not args.no_dispatch_sweep:
+        disp = {}
+        for N, L in ((1024, 1), (512, 4), (256, 8), (128, 16), (64, 32), (16, 256),
+                     (2, 2048)):
+            w = wp.replace(seq_len=L, n_seqs=N, seed=wp.seed + 11)
+            y = synth.make(w)
+            t = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in y.items()}
+            o = torch.empty((N * L, w.hv, w.d), dtype=torch.bfloat16, device=dev)
+            fs = torch.empty((N, w.hv, w.d, w.d), device=dev)
+            ws = gdn.alloc_workspace(N, N * L, w.hqk, w.hv, w.d, gdn.CHUNK_AUTO, dev)
+            row = {"auto_chunk": gdn.prefill_auto_chunk(N, N * L, w.hqk, w.hv, w.d, w.d)}
+            for key, c in (("auto", gdn.CHUNK_AUTO), ("chunk64", 64)):
+                def call():
+                    gdn.prefill(t["q"], t["k"], t["v"], t["g"], t["beta"], t["cu_seqlens"],
+                                chunk=c, o=o, final_state=fs, workspace=ws)
+                for _ in range(3):
+                    call()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(20):
+                    call()
+                e1.record()
+                torch.cuda.synchronize()
+                row[key + "_us"] = round(e0.elapsed_time(e1) * 1e3 / 20, 2)
+            row["auto_tokens_per_s"] = round(N * L / (row["auto_us"] * 1e-6), 1)
+            disp["N%d_L%d" % (N, L)] = row
+            del t, o, fs, ws
+        out["prefill_dispatch"] = disp
 
     # ---------------------------------------------------------------- oracle
     if not args.no_cpu_baseline:

@@ -40,7 +40,8 @@
  * T_total, overlapping in/out buffers other than the aliases allowed below)
  * are undefined behaviour. NaN and Inf propagate without checks.
  *
- * Supported shapes: DK == DV in {32, 64, 128}; chunk in {16, 32, 64}.
+ * Supported shapes: DK == DV in {32, 64, 128}; chunk in {0 (automatic), 1
+ * (token-serial), 16, 32, 64}.
  */
 #ifndef GDN_H_
 #define GDN_H_
@@ -67,6 +68,18 @@ typedef enum gdn_dtype {
   GDN_F32 = 1   /* q, k, v, o are float32                                 */
 } gdn_dtype;
 
+/*
+ * Flag OR-ed into the `chunk` argument of gdn_prefill, gdn_prefill_gated and
+ * gdn_prefill_workspace_size together with a chunk size of 16, 32 or 64: the
+ * 16 x 16 diagonal blocks of the WY factor (I + A)^-1 are formed by the
+ * Neumann series in its product form, (I - N)(I + N^2)(I + N^4)(I + N^8) for
+ * a strictly lower block N, on the matrix cores (the chunk-solve variant of
+ * the paper's Section 5.1), instead of by forward substitution. Same result
+ * up to rounding; the workspace is the same. Any other combination returns
+ * GDN_ERR_UNSUPPORTED (0 from gdn_prefill_workspace_size).
+ */
+#define GDN_CHUNK_NEUMANN 0x100
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char *gdn_status_string(gdn_status status);
 
@@ -75,12 +88,26 @@ int gdn_version(void);
 
 /*
  * Bytes of device workspace gdn_prefill needs for these sizes (0 on invalid
- * sizes). The bound depends on N and T_total only through ceil(T_total/chunk)
- * + N, so a caller may size it once for the largest batch it will submit.
+ * sizes). The size grows with N and T_total, so a caller may size it once for
+ * the largest batch it will submit. chunk = 1 needs no workspace and reports
+ * the 256-byte minimum; chunk = 0 reports the largest size over every choice
+ * the automatic dispatch can make, so it also covers every smaller batch.
  */
 size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
                                   int32_t hqk, int32_t hv, int32_t dk,
                                   int32_t dv, int32_t chunk);
+
+/*
+ * The chunk size gdn_prefill uses when called with chunk = 0 for these
+ * sizes: 1 (token-serial), 16, 32 or 64; 0 on invalid sizes. Shape dispatch
+ * after the paper's Sections 5.1 and 5.2: the choice depends on the head size
+ * and the average sequence length T_total / N (rounded up), with bounds
+ * measured on MI355X. Very short sequences take the token-serial path, where
+ * the chunked form's per-chunk work does not pay; longer ones take 16, 32 or
+ * 64 as the average length grows. Pure host function; no HIP call.
+ */
+int32_t gdn_prefill_auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hqk,
+                               int32_t hv, int32_t dk, int32_t dv);
 
 /*
  * Chunked prefill over N packed variable-length sequences (paper, Sections
@@ -91,6 +118,11 @@ size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
  * not the result. Per chunk, the intra-chunk recurrence is summarised by a
  * unit lower-triangular WY factor; the state is carried chunk to chunk in
  * float32.
+ *
+ * chunk = 1 runs the token-serial form instead: the recurrence token by
+ * token in float32 on the vector ALU, the state held in registers for the
+ * whole sequence (a short-sequence path, paper Section 5.2). chunk = 0 picks
+ * one of the sizes as gdn_prefill_auto_chunk() reports.
  *
  *   q, k, v, g, beta, cu_seqlens : inputs, layouts above.
  *   initial_state : [N, HV, DV, DK] float32, or NULL for zero states.

@@ -107,25 +107,12 @@ static hipError_t launch_decode_p(const DecodeArgs &a, int64_t total_rows) {
   return hipGetLastError();
 }
 
-// Compute units of the current device, read once per process.
-static int device_cus() {
-  static const int cus = [] {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        n <= 0)
-      n = 256;
-    return n;
-  }();
-  return cus;
-}
-
 template <int D, typename TIn>
 static hipError_t launch_decode_t(const DecodeArgs &a) {
   const int64_t total_rows = (int64_t)a.batch * a.hv * D;
   if (total_rows == 0) return hipSuccess;
   const int64_t blocks4 = (total_rows + (kWave / (D / 4)) * 16 - 1) / ((kWave / (D / 4)) * 16);
-  if (blocks4 < 2 * (int64_t)device_cus()) return launch_decode_p<D, 2, TIn>(a, total_rows);
+  if (blocks4 < 2 * (int64_t)device_compute_units()) return launch_decode_p<D, 2, TIn>(a, total_rows);
   return launch_decode_p<D, 4, TIn>(a, total_rows);
 }
 

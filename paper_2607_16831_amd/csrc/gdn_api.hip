@@ -7,17 +7,74 @@
 #include "../../include/gdn.h"
 #include "gdn_launch.h"
 
+namespace gdn {
+
+int device_compute_units() {
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    return n;
+  }();
+  return cus;
+}
+
+}  // namespace gdn
+
 namespace {
 
 bool supported_head(int32_t dk, int32_t dv) {
   return dk == dv && (dk == 32 || dk == 64 || dk == 128);
 }
-bool supported_chunk(int32_t c) { return c == 16 || c == 32 || c == 64; }
+// 1: token-serial path; 16, 32, 64: chunked path. 0 (automatic) is resolved
+// by auto_chunk() before this check.
+bool supported_chunk(int32_t c) { return c == 1 || c == 16 || c == 32 || c == 64; }
 bool supported_dtype(gdn_dtype t) { return t == GDN_BF16 || t == GDN_F32; }
 
 gdn_status check_heads(int32_t hqk, int32_t hv) {
   if (hqk <= 0 || hv <= 0 || hv % hqk != 0) return GDN_ERR_INVALID_ARG;
   return GDN_OK;
+}
+
+// Shape dispatch of the prefill (the paper's Section 5.1: the chunk size is
+// chosen from the number of sequences, the total tokens and the average
+// sequence length; Section 5.2: a narrow token-serial path for tiny shapes).
+// The rule is a table on the average length T/N per head size: up to
+// `serial` tokens the token-serial path, then chunks of 16, 32 and 64 up to
+// the next bounds. Bounds measured on MI355X (16 q/k and 32 v heads, bf16,
+// T = 1024 and 8192, lengths 1 to 8192): at every measured shape the chosen
+// path is within 10% of the fastest of the four, except where lengths fall
+// between two measured ones.
+struct ChunkRule {
+  int d, serial, c16, c32;  // largest average length for chunk 1, 16, 32
+};
+constexpr ChunkRule kChunkRules[] = {
+    {32, 40, 40, 112},    // chunk 16 never wins at d = 32
+    {64, 20, 20, 112},    // nor at d = 64
+    {128, 9, 20, 320},
+};
+
+int32_t auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t d) {
+  if (n_seqs <= 0) return 64;
+  ChunkRule r = kChunkRules[2];
+  for (const ChunkRule &c : kChunkRules)
+    if (c.d == d) r = c;
+  // average length, rounded up, compared with whole-token bounds
+  const int64_t avg = (n_tokens + n_seqs - 1) / n_seqs;
+  if (avg <= r.serial) return 1;
+  if (avg <= r.c16) return 16;
+  if (avg <= r.c32) return 32;
+  return 64;
+}
+
+// Workspace bytes for a resolved chunk size. The token-serial path uses none;
+// it reports the 256-byte minimum so that 0 keeps meaning "invalid sizes".
+size_t required_workspace(int32_t n_seqs, int64_t n_tokens, int32_t hqk, int32_t hv, int32_t d,
+                       int32_t chunk) {
+  if (chunk == 1) return 256;
+  return gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, d, chunk).total;
 }
 
 // The gate inputs: either g and beta, or all four raw inputs of the gated
@@ -37,15 +94,19 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
   if (n_seqs < 0 || n_tokens < 0 || n_tokens > INT32_MAX) return GDN_ERR_INVALID_ARG;
   if (check_heads(hqk, hv) != GDN_OK) return GDN_ERR_INVALID_ARG;
   if (dk <= 0 || dv <= 0) return GDN_ERR_INVALID_ARG;
-  if (!supported_head(dk, dv) || !supported_chunk(chunk) || !supported_dtype(dtype))
+  // GDN_CHUNK_NEUMANN selects the Neumann-product diagonal inverse of the
+  // chunked path; it is meaningless for the token-serial path.
+  const bool neumann = (chunk & GDN_CHUNK_NEUMANN) != 0;
+  chunk &= ~GDN_CHUNK_NEUMANN;
+  if (chunk == 0 && !neumann) chunk = auto_chunk(n_seqs, n_tokens, dk);
+  if (!supported_head(dk, dv) || !supported_chunk(chunk) || !supported_dtype(dtype) ||
+      (neumann && chunk < 16))
     return GDN_ERR_UNSUPPORTED;
   if (n_seqs == 0) return n_tokens == 0 ? GDN_OK : GDN_ERR_INVALID_ARG;
   if (!cu_seqlens || !final_state) return GDN_ERR_INVALID_ARG;
   if (n_tokens > 0 && (!q || !k || !v || !o || !gate_present(g, beta, gate)))
     return GDN_ERR_INVALID_ARG;
-  const gdn::PrefillWorkspace ws =
-      gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, dk, chunk);
-  if (!workspace || workspace_bytes < ws.total ||
+  if (!workspace || workspace_bytes < required_workspace(n_seqs, n_tokens, hqk, hv, dk, chunk) ||
       (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
     return GDN_ERR_WORKSPACE;
 
@@ -59,10 +120,15 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
   a.n_seqs = n_seqs;
   a.n_tokens = n_tokens;
   a.hqk = hqk; a.hv = hv; a.d = dk; a.chunk = chunk;
+  a.neumann = neumann;
   a.dtype = dtype;
   a.workspace = workspace;
   a.stream = stream;
-  return gdn::launch_prefill(a, ws) == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+  const hipError_t e =
+      chunk == 1 ? gdn::launch_prefill_serial(a)
+                 : gdn::launch_prefill(
+                       a, gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, dk, chunk));
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
 }
 
 gdn_status decode_impl(const void *q, const void *k, const void *v, const float *g,
@@ -104,15 +170,35 @@ const char *gdn_status_string(gdn_status status) {
   return "unknown status";
 }
 
-int gdn_version(void) { return 1 * 10000 + 1 * 100 + 0; }
+int gdn_version(void) { return 1 * 10000 + 2 * 100 + 0; }
 
 size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
                                   int32_t hqk, int32_t hv, int32_t dk,
                                   int32_t dv, int32_t chunk) {
   if (n_seqs < 0 || n_tokens < 0 || n_tokens > INT32_MAX) return 0;
   if (check_heads(hqk, hv) != GDN_OK) return 0;
-  if (!supported_head(dk, dv) || !supported_chunk(chunk)) return 0;
-  return gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, dk, chunk).total;
+  if (!supported_head(dk, dv)) return 0;
+  if (chunk & GDN_CHUNK_NEUMANN) {  // same tables as the plain chunked path
+    chunk &= ~GDN_CHUNK_NEUMANN;
+    if (chunk < 16) return 0;
+  }
+  if (chunk == 0) {  // enough for whichever size the dispatch picks
+    size_t m = 0;
+    for (int32_t c : {1, 16, 32, 64}) {
+      const size_t b = required_workspace(n_seqs, n_tokens, hqk, hv, dk, c);
+      m = b > m ? b : m;
+    }
+    return m;
+  }
+  if (!supported_chunk(chunk)) return 0;
+  return required_workspace(n_seqs, n_tokens, hqk, hv, dk, chunk);
+}
+
+int32_t gdn_prefill_auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hqk, int32_t hv,
+                               int32_t dk, int32_t dv) {
+  if (n_seqs < 0 || n_tokens < 0 || n_tokens > INT32_MAX) return 0;
+  if (check_heads(hqk, hv) != GDN_OK || !supported_head(dk, dv)) return 0;
+  return auto_chunk(n_seqs, n_tokens, dk);
 }
 
 gdn_status gdn_prefill(const void *q, const void *k, const void *v,

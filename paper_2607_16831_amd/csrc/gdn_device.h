@@ -175,11 +175,35 @@ __device__ __forceinline__ float gate_log_decay(float a, float a_log, float dt_b
 __device__ __forceinline__ float gate_beta(float b) { return 1.f / (1.f + __expf(-b)); }
 
 // ---------------------------------------------------------------- reductions
-// Sum over aligned groups of `W` consecutive lanes (W a power of two <= 64).
+// Lane move of a DPP control within each 16-lane row (every lane has a source).
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+
+// Sum over aligned groups of `W` consecutive lanes (W a power of two <= 64);
+// every lane of a group receives the same total. Inside a 16-lane row the
+// partial sums move by DPP (quad swaps of 1 and 2 lanes, then the 8-lane and
+// 16-lane mirrors, each pairing a lane with one from the other half of its
+// group); across rows by the gfx950 row swaps, which exchange rows 0 <-> 1
+// and 2 <-> 3 (16 lanes) or the two 32-lane halves. No LDS instruction is used.
 template <int W>
 __device__ __forceinline__ float group_sum(float x) {
-#pragma unroll
-  for (int m = W / 2; m >= 1; m >>= 1) x += __shfl_xor(x, m, kWave);
+  static_assert(W >= 2 && W <= kWave && (W & (W - 1)) == 0, "group width");
+  x += dpp_move<0xB1>(x);                      // quad_perm [1,0,3,2]
+  if constexpr (W >= 4) x += dpp_move<0x4E>(x);   // quad_perm [2,3,0,1]
+  if constexpr (W >= 8) x += dpp_move<0x141>(x);  // row_half_mirror
+  if constexpr (W >= 16) x += dpp_move<0x140>(x); // row_mirror
+  if constexpr (W >= 32) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  if constexpr (W >= 64) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
   return x;
 }
 

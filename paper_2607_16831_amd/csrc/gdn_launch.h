@@ -37,6 +37,7 @@ struct PrefillArgs {
   int n_seqs;
   int64_t n_tokens;
   int hqk, hv, d, chunk;
+  bool neumann;  // diagonal blocks of the WY factor by the Neumann product
   gdn_dtype dtype;
   void *workspace;
   hipStream_t stream;
@@ -65,6 +66,12 @@ PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
                                           int hv, int d, int chunk);
 
 hipError_t launch_decode(const DecodeArgs &a);
+// Chunked prefill (chunk 16, 32 or 64) and the token-serial prefill (chunk 1,
+// no workspace).
 hipError_t launch_prefill(const PrefillArgs &a, const PrefillWorkspace &ws);
+hipError_t launch_prefill_serial(const PrefillArgs &a);
+
+// Compute units of the current device, read once per process.
+int device_compute_units();
 
 }  // namespace gdn

@@ -97,9 +97,11 @@ typedef __attribute__((address_space(3))) void lds_void;
 // evenly: wavefront w computes product (w & 1) (0: K K^T for A, 1: K Q^T
 // for P) for the block rows of row set (w >> 1).
 //
-// T is built from its 16x16 blocks in fp32. Diagonal block b is inverted by
-// forward substitution on the vector ALU (one lane per column, all blocks at
-// once in one wavefront); wavefront b then forms its block row from
+// T is built from its 16x16 blocks in fp32. Diagonal block b is inverted
+// either by forward substitution on the vector ALU (one lane per column, all
+// blocks at once in one wavefront) or, with NEUMANN, by the Neumann product
+// on the matrix cores (one block per wavefront, see neumann_diag); wavefront
+// b then forms its block row from
 //   T[b][c] = -(sum_{m=c+1..b} T[b][m] A[m][c]) T[c][c]^-1    (c < b),
 // carried in transposed form so that every intermediate stays in the
 // accumulator layout of the fp32 16x16x4 matrix instruction.
@@ -127,7 +129,45 @@ __device__ __forceinline__ int gram_row(int p, int r) {
   return NIB == 4 ? p : -1;
 }
 
-template <int D, int C, typename TIn>
+// Inverse of one unit lower-triangular 16 x 16 block I + N by the Neumann
+// series, exact because N is strictly lower and so N^16 = 0, in its product
+// form (the chunk-solve variant the paper's Section 5.1 names):
+//   (I + N)^-1 = (I - N)(I + N^2)(I + N^4)(I + N^8).
+// One wavefront, fp32 16x16x4 matrix instructions. Matrices are held in the
+// accumulator layout (lane (g, n) holds rows 4g..4g+3 of column n); a
+// product X Y takes Y in that layout as its B operand and X^T in that layout
+// as its A operand, so each power is carried with its transpose and no data
+// moves between products: P^2 = mul(P^T, P) and (P^2)^T = mul(P, P^T). The
+// factors commute, so each is applied from the left. Ab: the block in LDS,
+// row-major with pitch AP; the inverse is returned in the accumulator layout.
+template <int AP>
+__device__ __forceinline__ f32x4 neumann_diag(const float *Ab, int g4, int l16) {
+  auto mul = [](f32x4 at, f32x4 b) {  // (matrix of at)^T times (matrix of b)
+    f32x4 r = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) r = mfma_16x16x4_f32(at[kk], b[kk], r);
+    return r;
+  };
+  f32x4 eye, P, Pt;  // P = (-N)^(2^k) and its transpose
+  const float4 nt = *reinterpret_cast<const float4 *>(&Ab[l16 * AP + 4 * g4]);
+  Pt = f32x4{-nt.x, -nt.y, -nt.z, -nt.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    eye[e] = (4 * g4 + e == l16) ? 1.f : 0.f;
+    P[e] = -Ab[(4 * g4 + e) * AP + l16];
+  }
+  f32x4 inv = eye + P;  // I - N
+#pragma unroll
+  for (int k = 1; k < 4; ++k) {
+    const f32x4 P2 = mul(Pt, P), P2t = mul(P, Pt);
+    P = P2;
+    Pt = P2t;
+    inv = mul(eye + Pt, inv);  // (I + N^(2^k)) times the product so far
+  }
+  return inv;
+}
+
+template <int D, int C, typename TIn, bool NEUMANN>
 __global__ __launch_bounds__(256) void chunk_local_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k,
     const float *__restrict__ g, const float *__restrict__ beta, GateArgs gate,
@@ -348,10 +388,17 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   }
   lds_barrier();
 
-  // ---- diagonal blocks by forward substitution: lane (b, c) = (g4, l16)
-  // solves (I + A[b][b]) x = e_c, i.e. column c of T[b][b], and stores it as
-  // row c of the transposed inverse.
-  if (wave == 0) {
+  // ---- diagonal blocks. Neumann product: wavefront b inverts block b and
+  // stores it transposed (linv[b] row c = column c of the inverse).
+  if (NEUMANN && wave < NIB) {
+    const f32x4 tb = neumann_diag<AP>(L.u.inv.A[wave * (wave + 1) / 2 + wave], g4, l16);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) L.u.inv.linv[wave][l16 * 17 + 4 * g4 + e] = tb[e];
+  }
+  // Forward substitution: lane (b, c) = (g4, l16) solves (I + A[b][b]) x =
+  // e_c, i.e. column c of T[b][b], and stores it as row c of the transposed
+  // inverse.
+  if (!NEUMANN && wave == 0) {
     const int b = min(g4, NIB - 1);  // lanes past the last block repeat it
     const float *Ab = L.u.inv.A[b * (b + 1) / 2 + b];
     float x[16];
@@ -1007,8 +1054,9 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
     // (chunk, key head) pairs in groups of eight, times the heads of a group.
     const int64_t pairs = nc * a.hqk;
     const int64_t lblocks = ((pairs + 7) / 8) * 8 * group;
-    hipLaunchKernelGGL((chunk_local_kernel<D, C, TIn>), dim3((unsigned)lblocks), dim3(256), 0,
-                       a.stream, (const TIn *)a.q, (const TIn *)a.k, a.g, a.beta, a.gate,
+    auto local = a.neumann ? chunk_local_kernel<D, C, TIn, true>
+                           : chunk_local_kernel<D, C, TIn, false>;
+    hipLaunchKernelGGL(local, dim3((unsigned)lblocks), dim3(256), 0, a.stream, (const TIn *)a.q, (const TIn *)a.k, a.g, a.beta, a.gate,
                        a.cu_seqlens, a.n_seqs, a.hqk, a.hv, group, (int)pairs, dec, tf, pf,
                        qf, kc);
     const hipError_t e = hipGetLastError();

@@ -20,7 +20,15 @@ GDN_OK, GDN_ERR_INVALID_ARG, GDN_ERR_UNSUPPORTED, GDN_ERR_WORKSPACE, GDN_ERR_HIP
 GDN_BF16, GDN_F32 = 0, 1
 
 EXPORTS = ("gdn_status_string", "gdn_version", "gdn_prefill_workspace_size",
-           "gdn_prefill", "gdn_decode", "gdn_prefill_gated", "gdn_decode_gated")
+           "gdn_prefill_auto_chunk", "gdn_prefill", "gdn_decode", "gdn_prefill_gated",
+           "gdn_decode_gated")
+
+# Prefill chunk sizes: AUTO lets the library choose from the batch shape,
+# SERIAL runs the token-serial path; 16, 32 and 64 run the chunked path.
+CHUNK_AUTO, CHUNK_SERIAL = 0, 1
+# OR-ed into a chunk size of 16, 32 or 64: diagonal blocks of the WY factor by
+# the Neumann product instead of forward substitution.
+CHUNK_NEUMANN = 0x100
 
 _lib = None
 
@@ -48,6 +56,8 @@ def lib() -> ctypes.CDLL:
         L.gdn_version.restype = ctypes.c_int
         L.gdn_prefill_workspace_size.argtypes = [i32, i64, i32, i32, i32, i32, i32]
         L.gdn_prefill_workspace_size.restype = sz
+        L.gdn_prefill_auto_chunk.argtypes = [i32, i64, i32, i32, i32, i32]
+        L.gdn_prefill_auto_chunk.restype = i32
         L.gdn_prefill.argtypes = [vp, vp, vp, fp, fp, ip, fp, vp, fp, i32, i64,
                                   i32, i32, i32, i32, i32, ctypes.c_int, vp, sz, vp]
         L.gdn_prefill.restype = ctypes.c_int
@@ -75,6 +85,11 @@ def version() -> int:
 
 def prefill_workspace_size(n_seqs, n_tokens, hqk, hv, dk, dv, chunk) -> int:
     return int(lib().gdn_prefill_workspace_size(n_seqs, n_tokens, hqk, hv, dk, dv, chunk))
+
+
+def prefill_auto_chunk(n_seqs, n_tokens, hqk, hv, dk, dv) -> int:
+    """Chunk size the library picks for chunk=CHUNK_AUTO (0 on invalid sizes)."""
+    return int(lib().gdn_prefill_auto_chunk(n_seqs, n_tokens, hqk, hv, dk, dv))
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -152,7 +167,11 @@ def prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor,
             final_state: Optional[torch.Tensor] = None,
             workspace: Optional[torch.Tensor] = None,
             stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Chunked prefill; returns (o [T, HV, DV], final_state [N, HV, DV, DK])."""
+    """Prefill; returns (o [T, HV, DV], final_state [N, HV, DV, DK]).
+
+    chunk: 16, 32 or 64 (chunked path), CHUNK_SERIAL (token-serial path) or
+    CHUNK_AUTO (the library's shape dispatch).
+    """
     T, hqk, dk = q.shape
     hv, dv = v.shape[1], v.shape[2]
     N = cu_seqlens.shape[0] - 1

@@ -54,6 +54,63 @@ def test_workspace_size():
     assert a >= (4096 // 64 + 1) * 32 * 64 * 64 * 4
 
 
+def test_workspace_size_serial_and_auto():
+    ws = gdn.prefill_workspace_size
+    # the token-serial path needs none and reports the 256-byte minimum
+    assert ws(64, 256, 16, 32, 128, 128, gdn.CHUNK_SERIAL) == 256
+    assert ws(0, 0, 16, 32, 128, 128, gdn.CHUNK_SERIAL) == 256
+    # automatic: the largest size over every choice, for any batch shape
+    for n, t in ((1, 4096), (64, 64), (4096, 4096), (16, 66000), (3, 7)):
+        auto = ws(n, t, 16, 32, 128, 128, gdn.CHUNK_AUTO)
+        for c in (1, 16, 32, 64):
+            assert auto >= ws(n, t, 16, 32, 128, 128, c)
+        assert auto in [ws(n, t, 16, 32, 128, 128, c) for c in (1, 16, 32, 64)]
+    assert ws(1, 4096, 16, 32, 96, 96, gdn.CHUNK_AUTO) == 0
+    assert ws(1, 4096, 16, 32, 128, 128, 2) == 0
+
+
+def test_neumann_flag_sizes_and_validation():
+    ws = gdn.prefill_workspace_size
+    N = gdn.CHUNK_NEUMANN
+    for c in (16, 32, 64):
+        assert ws(3, 1000, 2, 4, 64, 64, c | N) == ws(3, 1000, 2, 4, 64, 64, c)
+    assert ws(3, 1000, 2, 4, 64, 64, 1 | N) == 0
+    assert ws(3, 1000, 2, 4, 64, 64, 0 | N) == 0
+    assert ws(3, 1000, 2, 4, 64, 64, 48 | N) == 0
+    E = gdn
+    assert _prefill(chunk=1 | N) == E.GDN_ERR_UNSUPPORTED
+    assert _prefill(chunk=0 | N) == E.GDN_ERR_UNSUPPORTED
+    assert _prefill(chunk=48 | N) == E.GDN_ERR_UNSUPPORTED
+    assert _prefill(chunk=16 | N, workspace_bytes=0) == E.GDN_ERR_WORKSPACE
+    assert _prefill(chunk=16 | N, q=None) == E.GDN_ERR_INVALID_ARG
+
+
+def test_auto_chunk_rule():
+    ac = gdn.prefill_auto_chunk
+    picks = [ac(n, t, 16, 32, 128, 128) for n, t in
+             ((4096, 4096), (512, 2048), (128, 128 * 12), (64, 64 * 40), (1, 4096),
+              (16, 66000))]
+    # measured choices at d = 128: token-serial up to ~8 tokens, then 16, 32, 64
+    assert picks == [1, 1, 16, 32, 64, 64]
+    order = {1: 0, 16: 1, 32: 2, 64: 3}
+    for d in (32, 64, 128):
+        # every length maps to a built size, monotone in the average length
+        avg = [ac(64, 64 * L, 16, 32, d, d) for L in range(1, 1200)]
+        assert set(avg) <= {1, 16, 32, 64} and avg[0] == 1 and avg[-1] == 64
+        assert all(order[a] <= order[b] for a, b in zip(avg, avg[1:]))
+        # the average is rounded up: 64 sequences of 8 and one of 9 tokens
+        # count as 9
+        assert ac(65, 64 * 8 + 9, 16, 32, d, d) == ac(1, 9, 16, 32, d, d)
+    # smaller heads keep the token-serial path longer (it costs 6 d^2 per token)
+    serial_max = {d: max(L for L in range(1, 200) if ac(1, L, 1, 1, d, d) == 1)
+                  for d in (32, 64, 128)}
+    assert serial_max[32] >= serial_max[64] >= serial_max[128]
+    assert ac(0, 0, 16, 32, 128, 128) in (1, 16, 32, 64)
+    assert ac(-1, 0, 16, 32, 128, 128) == 0
+    assert ac(1, 64, 16, 24, 128, 128) == 0
+    assert ac(1, 64, 16, 32, 96, 96) == 0
+
+
 def _prefill(**kw):
     args = dict(q=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE, cu_seqlens=FAKE,
                 initial_state=None, o=FAKE, final_state=FAKE, n_seqs=1,
@@ -72,6 +129,14 @@ def test_prefill_validation():
     assert _prefill(dk=128, dv=64) == E.GDN_ERR_UNSUPPORTED
     assert _prefill(dk=96, dv=96) == E.GDN_ERR_UNSUPPORTED
     assert _prefill(chunk=48) == E.GDN_ERR_UNSUPPORTED
+    assert _prefill(chunk=2) == E.GDN_ERR_UNSUPPORTED
+    assert _prefill(chunk=-1) == E.GDN_ERR_UNSUPPORTED
+    # the token-serial path still takes a (256-byte) workspace argument
+    assert _prefill(chunk=gdn.CHUNK_SERIAL, workspace=None) == E.GDN_ERR_WORKSPACE
+    assert _prefill(chunk=gdn.CHUNK_SERIAL, workspace_bytes=255) == E.GDN_ERR_WORKSPACE
+    assert _prefill(chunk=gdn.CHUNK_SERIAL, q=None, workspace_bytes=256) == \
+        E.GDN_ERR_INVALID_ARG
+    assert _prefill(chunk=gdn.CHUNK_AUTO, workspace_bytes=255) == E.GDN_ERR_WORKSPACE
     assert _prefill(dtype=7) == E.GDN_ERR_UNSUPPORTED
     assert _prefill(q=None) == E.GDN_ERR_INVALID_ARG
     assert _prefill(cu_seqlens=None) == E.GDN_ERR_INVALID_ARG
