@@ -51,7 +51,7 @@ struct ChunkRule {
   int d, serial, c16, c32;  // largest average length for chunk 1, 16, 32
 };
 constexpr ChunkRule kChunkRules[] = {
-    {32, 40, 40, 112},    // chunk 16 never wins at d = 32
+    {32, 48, 48, 112},    // chunk 16 never wins at d = 32
     {64, 20, 20, 112},    // nor at d = 64
     {128, 9, 20, 320},
 };
