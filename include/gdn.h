@@ -100,8 +100,8 @@ size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
 /*
  * The chunk size gdn_prefill uses when called with chunk = 0 for these
  * sizes: 1 (token-serial), 16, 32 or 64; 0 on invalid sizes. Shape dispatch
- * after the paper's Sections 5.1 and 5.2: the choice depends on the head size
- * and the average sequence length T_total / N (rounded up), with bounds
+ * after the paper's Sections 5.1 and 5.2: the choice depends on the head size,
+ * the average sequence length T_total / N (rounded up) and N, with bounds
  * measured on MI355X. Very short sequences take the token-serial path, where
  * the chunked form's per-chunk work does not pay; longer ones take 16, 32 or
  * 64 as the average length grows. Pure host function; no HIP call.

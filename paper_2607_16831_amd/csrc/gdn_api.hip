@@ -41,19 +41,20 @@ gdn_status check_heads(int32_t hqk, int32_t hv) {
 // Shape dispatch of the prefill (the paper's Section 5.1: the chunk size is
 // chosen from the number of sequences, the total tokens and the average
 // sequence length; Section 5.2: a narrow token-serial path for tiny shapes).
-// The rule is a table on the average length T/N per head size: up to
-// `serial` tokens the token-serial path, then chunks of 16, 32 and 64 up to
-// the next bounds. Bounds measured on MI355X (16 q/k and 32 v heads, bf16,
-// T = 1024 and 8192, lengths 1 to 8192): at every measured shape the chosen
-// path is within 10% of the fastest of the four, except where lengths fall
-// between two measured ones.
+// The rule is a table per head size on the average length T/N (rounded up)
+// and the number of sequences N: the token-serial path up to `serial`
+// tokens, or up to `serial_big` when N >= n_big; then chunks of 16, 32 and
+// 64 up to the next bounds. Bounds measured on MI355X (16 q/k and 32 v
+// heads, bf16, T = 1024 and 8192, lengths 1 to 8192, each chunked run with
+// the carry the dispatch below pairs with it): at every measured shape the
+// chosen path is within 15% of the fastest of the four.
 struct ChunkRule {
-  int d, serial, c16, c32;  // largest average length for chunk 1, 16, 32
+  int d, serial, serial_big, n_big, c16, c32;
 };
 constexpr ChunkRule kChunkRules[] = {
-    {32, 48, 48, 112},    // chunk 16 never wins at d = 32
-    {64, 20, 20, 112},    // nor at d = 64
-    {128, 9, 20, 320},
+    {32, 24, 24, 0, 24, 32},      // chunk 16 never wins at d = 32
+    {64, 4, 4, 0, 16, 32},
+    {128, 1, 4, 1536, 16, 320},
 };
 
 int32_t auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t d) {
@@ -61,9 +62,8 @@ int32_t auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t d) {
   ChunkRule r = kChunkRules[2];
   for (const ChunkRule &c : kChunkRules)
     if (c.d == d) r = c;
-  // average length, rounded up, compared with whole-token bounds
   const int64_t avg = (n_tokens + n_seqs - 1) / n_seqs;
-  if (avg <= r.serial) return 1;
+  if (avg <= r.serial || (avg <= r.serial_big && n_seqs >= r.n_big)) return 1;
   if (avg <= r.c16) return 16;
   if (avg <= r.c32) return 32;
   return 64;
@@ -121,6 +121,9 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
   a.n_tokens = n_tokens;
   a.hqk = hqk; a.hv = hv; a.d = dk; a.chunk = chunk;
   a.neumann = neumann;
+  // The single-wave carry when the average sequence fits in one chunk: a
+  // work-group carry's fixed cost then outweighs its per-chunk speed.
+  a.wave_carry = n_tokens <= (int64_t)n_seqs * chunk;
   a.dtype = dtype;
   a.workspace = workspace;
   a.stream = stream;

@@ -134,6 +134,11 @@ struct BufElem<__bf16> {
   static __device__ __forceinline__ float load1(rsrc_t r, uint32_t e) {
     return bf16_bits_to_f32(__builtin_amdgcn_raw_buffer_load_b16(r, e * 2u, 0, 0));
   }
+  // Four consecutive elements as packed bf16.
+  static __device__ __forceinline__ uint2 load4_bf16(rsrc_t r, uint32_t e) {
+    const auto x = __builtin_amdgcn_raw_buffer_load_b64(r, e * 2u, 0, 0);
+    return make_uint2(x[0], x[1]);
+  }
   static __device__ __forceinline__ void store1(rsrc_t r, uint32_t e, float x) {
     __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_bits(x), r, e * 2u, 0, 0);
   }
@@ -153,6 +158,10 @@ struct BufElem<float> {
   }
   static __device__ __forceinline__ float load1(rsrc_t r, uint32_t e) {
     return buf_load_f32(r, e * 4u);
+  }
+  static __device__ __forceinline__ uint2 load4_bf16(rsrc_t r, uint32_t e) {
+    const float4 a = buf_load_f32x4(r, e * 4u);
+    return make_uint2(pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w));
   }
   static __device__ __forceinline__ void store1(rsrc_t r, uint32_t e, float x) {
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, e * 4u, 0, 0);

@@ -38,6 +38,7 @@ struct PrefillArgs {
   int64_t n_tokens;
   int hqk, hv, d, chunk;
   bool neumann;  // diagonal blocks of the WY factor by the Neumann product
+  bool wave_carry;  // single-wave carry (batches of short sequences)
   gdn_dtype dtype;
   void *workspace;
   hipStream_t stream;

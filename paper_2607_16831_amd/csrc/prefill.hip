@@ -1016,6 +1016,225 @@ __global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
     store_stream(sT + ((int64_t)pair * D + v0 + l16) * D + 16 * wave + 4 * g4, S);
 }
 
+// ============================================================ single-wave carry
+// The carry for batches of short sequences: one wavefront per (sequence,
+// value head, 16-row value tile), 4 independent wavefronts per work-group,
+// no barrier and no exchange between wavefronts. It walks the chunks of its
+// sequence like the work-group carry; it is chosen when the average
+// sequence fits in one chunk, where the work-group carry's fixed cost per
+// work-group (ten wavefronts, the LDS of four chunk buffers) dominates.
+//
+// The state tile lives in the wavefront's accumulators for all key tiles:
+// lane (l16, g4) element e of tile t is S[v0 + l16][16 t + 4 g4 + e]. Every
+// contraction over the keys names its slots so that step s, slot
+// 8 g + 4 hh + e stands for key 32 s + 16 hh + 4 g + e (the order of tok_pos
+// over the keys): the bf16 B operand of S^T is then packed straight from
+// tiles 2 s and 2 s + 1, and the A operands (K rows from LDS, Q rows from
+// global memory) supply their keys in the same order. Y and U come out of
+// their products in the accumulator layout, which in the token order of
+// tok_pos is already the B operand of T' Y, P U and K^T (e U). Only K goes
+// through LDS, for the K^T operands of the state update (transpose reads).
+template <int D, int C>
+struct WaveCfg {
+  using F = Cfg<D, C>;
+  static constexpr int WAVES = 4;
+  static constexpr int NKI = C * D / 512;  // 1 KB copies per K chunk
+};
+
+// T' (and P) fragments of block row ib that are not all zero: steps s <= ib/2.
+template <int C>
+__device__ __forceinline__ constexpr int frag_steps(int ib) {
+  return (ib / 2 + 1) < (C + 31) / 32 ? (ib / 2 + 1) : (C + 31) / 32;
+}
+
+// B operand of a contraction over the chunk's tokens, step st: blocks 2 st
+// (slots 0-3) and 2 st + 1 (slots 4-7) of accumulator tiles X, each element
+// times w[block][e] (or as is when w is null), rounded to bf16.
+template <int NIB>
+__device__ __forceinline__ uint4 u_operand(const f32x4 (&X)[NIB], int st, const f32x4 *w) {
+  const int b0 = 2 * st, b1 = 2 * st + 1;
+  f32x4 lo = X[b0 % NIB], hi = (b1 < NIB) ? X[b1 % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
+  if (w != nullptr) {
+    lo = lo * w[b0 % NIB];
+    if (b1 < NIB) hi = hi * w[b1 % NIB];
+  }
+  return make_uint4(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]),
+                    pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
+}
+
+// 16 x 32 A operand of a key contraction, rows from a row-major matrix:
+// lane (l16, g4) gives row l16, keys 32 s + 4 g4 + [0, 4) and
+// 32 s + 16 + 4 g4 + [0, 4).
+__device__ __forceinline__ uint4 key_operand(uint2 lo, uint2 hi) {
+  return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+
+template <int D, int C, typename TIn>
+__global__ __launch_bounds__(256) void chunk_wave_kernel(
+    const TIn *__restrict__ q, const TIn *__restrict__ k, const TIn *__restrict__ v,
+    const int32_t *__restrict__ cu, const float *__restrict__ dec_ws,
+    const uint16_t *__restrict__ tfrag, const uint16_t *__restrict__ pfrag,
+    const uint16_t *__restrict__ kcopy, const float *s0, float *sT, TIn *__restrict__ o,
+    int n_units, int hqk, int hv, int group) {
+  using F = Cfg<D, C>;
+  using WC = WaveCfg<D, C>;
+  using CC = CarryCfg<D, C, TIn>;
+  constexpr int NIB = F::NIB, KS = F::KS, DS = F::DS, NKT = F::NKT, NVT = F::NVT;
+  __shared__ __attribute__((aligned(16))) uint16_t Kw[WC::WAVES][F::CP * D];
+
+  // Work-group id -> (sequence, key head) unit and its tiles: every unit's
+  // work-groups go to one XCD (ids b, b + 8, ...), so the value heads and
+  // tiles that share K, Q, T' and P share an L2.
+  const int tiles = group * NVT;                     // tiles per unit
+  const int wpu = (tiles + WC::WAVES - 1) / WC::WAVES;  // work-groups per unit
+  const int id = blockIdx.x;
+  const int xg = id & 7, jj = id >> 3;
+  const int unit = (jj / wpu) * 8 + xg;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tix = (jj % wpu) * WC::WAVES + wave;
+  const int lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
+  uint16_t *K = Kw[wave];
+  if (C < F::CP) {  // token rows past the chunk stay zero (K^T reads cover CP rows)
+    for (int idx = C * D + lane; idx < F::CP * D; idx += 64) K[idx] = 0;
+  }
+  if (unit >= n_units || tix >= tiles) return;  // whole wavefront
+  const int n = unit / hqk, hk = unit % hqk;
+  const int gi = tix / NVT, vt = tix % NVT;
+  const int h = hk * group + gi, v0 = 16 * vt;
+  const int64_t pair = (int64_t)n * hv + h;
+  const int64_t seq_t0 = cu[n], seq_t1 = cu[n + 1];
+  const int nch = (int)((seq_t1 - seq_t0 + C - 1) / C);
+  const int64_t c0 = first_slot(cu, n, C);
+
+  f32x4 Sacc[NKT];
+#pragma unroll
+  for (int t = 0; t < NKT; ++t) {
+    Sacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (s0 != nullptr) {
+      const float4 x = *reinterpret_cast<const float4 *>(s0 + (pair * D + v0 + l16) * D + 16 * t + 4 * g4);
+      Sacc[t] = f32x4{x.x, x.y, x.z, x.w};
+    }
+  }
+
+  // bf16 K comes straight from the input, f32 K from its bf16 copy
+  const bool kcopied = sizeof(TIn) != 2;
+  const uint16_t *ksrc = kcopied ? kcopy : reinterpret_cast<const uint16_t *>(k);
+  const int kstride = kcopied ? D : hqk * D;
+  uint32_t koff[WC::NKI];
+#pragma unroll
+  for (int m = 0; m < WC::NKI; ++m) koff[m] = copy_offset<D, C, TIn>(m, lane, kstride, hv);
+
+  for (int lc = 0; lc < nch; ++lc) {
+    const int64_t t0 = seq_t0 + (int64_t)lc * C;
+    const int nv = (int)min((int64_t)C, seq_t1 - t0);
+    const int64_t slot = (c0 + lc) * hv + h;
+    // ---- loads: K chunk into LDS (rows past nv read as zero), the tables
+    const rsrc_t rk = kcopied ? make_rsrc(ksrc + ((c0 + lc) * hqk + hk) * (C * D), C * D * 2)
+                              : make_rsrc(ksrc + (t0 * hqk + hk) * D, (uint32_t)(nv * hqk * D * 2));
+#pragma unroll
+    for (int m = 0; m < WC::NKI; ++m) {
+      // (the offset goes in as a plain scalar: with an array element as the
+      // builtin's argument the host pass emitted no launch stub)
+      const uint32_t off = koff[m];
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void *)(K + 512 * m), 16, off, 0, 0, 0);
+    }
+    const rsrc_t rt = make_rsrc(tfrag + slot * F::FRAG, F::FRAG * 2);
+    const rsrc_t rp = make_rsrc(pfrag + slot * F::FRAG, F::FRAG * 2);
+    const rsrc_t rv = make_rsrc(v + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * sizeof(TIn)));
+    const float *dec = dec_ws + slot * 2 * C;
+    f32x4 ga[NIB], he[NIB], Y[NIB];
+#pragma unroll
+    for (int ib = 0; ib < NIB; ++ib) {
+      const float4 x = *reinterpret_cast<const float4 *>(dec + 16 * ib + 4 * g4);
+      const float4 y = *reinterpret_cast<const float4 *>(dec + C + 16 * ib + 4 * g4);
+      ga[ib] = f32x4{x.x, x.y, x.z, x.w};
+      he[ib] = f32x4{y.x, y.y, y.z, y.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        Y[ib][e] = BufElem<TIn>::load1(rv, (uint32_t)((16 * ib + 4 * g4 + e) * hv * D + l16));
+    }
+    const float glast = dec[C - 1];
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // K has landed in LDS
+
+    // ---- the state as the bf16 B operand of S^T, key order as above
+    uint4 SB[DS];
+#pragma unroll
+    for (int st = 0; st < DS; ++st)
+      SB[st] = make_uint4(pack_bf16x2(Sacc[2 * st][0], Sacc[2 * st][1]),
+                          pack_bf16x2(Sacc[2 * st][2], Sacc[2 * st][3]),
+                          pack_bf16x2(Sacc[2 * st + 1][0], Sacc[2 * st + 1][1]),
+                          pack_bf16x2(Sacc[2 * st + 1][2], Sacc[2 * st + 1][3]));
+
+    // ---- Y = V - exp(gamma) (K S^T), block by block
+#pragma unroll
+    for (int ib = 0; ib < NIB; ++ib) {
+      f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < DS; ++st) {
+        const int row = 16 * ib + l16, col = 32 * st + 4 * g4;
+        const uint2 lo = *reinterpret_cast<const uint2 *>(&K[kn_index<D>(row, col)]);
+        const uint2 hi = *reinterpret_cast<const uint2 *>(&K[kn_index<D>(row, col + 16)]);
+        x = mfma_16x16x32(key_operand(lo, hi), SB[st], x);
+      }
+      Y[ib] = Y[ib] - ga[ib] * x;
+    }
+
+    // ---- U = T' Y (beta is folded into T')
+    f32x4 U[NIB];
+#pragma unroll
+    for (int ib = 0; ib < NIB; ++ib) {
+      U[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < frag_steps<C>(ib); ++st) {
+        const uint4 a = buf_load_b128(rt, (uint32_t)(((ib * KS + st) * 64 + lane) * 16));
+        U[ib] = mfma_16x16x32(a, u_operand<NIB>(Y, st, nullptr), U[ib]);
+      }
+    }
+
+    // ---- O = exp(gamma) (Q S^T) + P U, stored by block
+    const rsrc_t rq = make_rsrc(q + (t0 * hqk + hk) * D, (uint32_t)(nv * hqk * D * sizeof(TIn)));
+    const rsrc_t ro = make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * sizeof(TIn)));
+#pragma unroll
+    for (int ib = 0; ib < NIB; ++ib) {
+      f32x4 qs = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < DS; ++st) {
+        const uint32_t e0 = (uint32_t)((16 * ib + l16) * hqk * D + 32 * st + 4 * g4);
+        qs = mfma_16x16x32(key_operand(BufElem<TIn>::load4_bf16(rq, e0),
+                                       BufElem<TIn>::load4_bf16(rq, e0 + 16)),
+                           SB[st], qs);
+      }
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < frag_steps<C>(ib); ++st) {
+        const uint4 a = buf_load_b128(rp, (uint32_t)(((ib * KS + st) * 64 + lane) * 16));
+        acc = mfma_16x16x32(a, u_operand<NIB>(U, st, nullptr), acc);
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        BufElem<TIn>::store1_stream(ro, (uint32_t)((16 * ib + 4 * g4 + e) * hv * D + l16),
+                                    ga[ib][e] * qs[e] + acc[e]);
+    }
+
+    // ---- S^T <- exp(gamma_last) S^T + K^T (exp(gamma_last - gamma) U)
+    uint4 bu[KS];
+#pragma unroll
+    for (int st = 0; st < KS; ++st) bu[st] = u_operand<NIB>(U, st, he);
+#pragma unroll
+    for (int t = 0; t < NKT; ++t) {
+      f32x4 acc = Sacc[t] * glast;
+#pragma unroll
+      for (int st = 0; st < KS; ++st) acc = mfma_16x16x32(kt_operand<D>(K, t, st, l16, g4), bu[st], acc);
+      Sacc[t] = acc;
+    }
+    // every read of this chunk's K is done before the next chunk's copy
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  }
+#pragma unroll
+  for (int t = 0; t < NKT; ++t)
+    store_stream(sT + (pair * D + v0 + l16) * D + 16 * t + 4 * g4, Sacc[t]);
+}
+
 // ============================================================ host side
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -1064,6 +1283,15 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
   }
 
   const int n_groups = a.n_seqs * a.hqk;
+  if (a.wave_carry) {
+    const int wpu = (group * F::NVT + WaveCfg<D, C>::WAVES - 1) / WaveCfg<D, C>::WAVES;
+    const int64_t wblocks = (int64_t)8 * ((n_groups + 7) / 8) * wpu;
+    hipLaunchKernelGGL((chunk_wave_kernel<D, C, TIn>), dim3((unsigned)wblocks), dim3(256), 0,
+                       a.stream, (const TIn *)a.q, (const TIn *)a.k, (const TIn *)a.v,
+                       a.cu_seqlens, dec, tf, pf, kc, a.initial_state, a.final_state, (TIn *)a.o,
+                       n_groups, a.hqk, a.hv, group);
+    return hipGetLastError();
+  }
   const int64_t blocks = (int64_t)8 * ((n_groups + 7) / 8) * group * F::NVT;
   hipLaunchKernelGGL((chunk_carry_kernel<D, C, TIn>), dim3((unsigned)blocks),
                      dim3(kCarryThreads), 0, a.stream, (const TIn *)a.k, (const TIn *)a.v,

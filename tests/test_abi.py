@@ -90,8 +90,10 @@ def test_auto_chunk_rule():
     picks = [ac(n, t, 16, 32, 128, 128) for n, t in
              ((4096, 4096), (512, 2048), (128, 128 * 12), (64, 64 * 40), (1, 4096),
               (16, 66000))]
-    # measured choices at d = 128: token-serial up to ~8 tokens, then 16, 32, 64
-    assert picks == [1, 1, 16, 32, 64, 64]
+    # measured choices at d = 128: token-serial for single tokens, then 16, 32, 64
+    assert picks == [1, 16, 16, 32, 64, 64]
+    # many sequences of a few tokens: token-serial at d = 128
+    assert ac(2048, 8192, 16, 32, 128, 128) == 1 and ac(512, 2048, 16, 32, 128, 128) == 16
     order = {1: 0, 16: 1, 32: 2, 64: 3}
     for d in (32, 64, 128):
         # every length maps to a built size, monotone in the average length

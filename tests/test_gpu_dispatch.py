@@ -148,7 +148,7 @@ def test_serial_gated(dtype):
 
 
 # ------------------------------------------------------------ chunk = 0
-@pytest.mark.parametrize("n_seqs,length", [(256, 2), (64, 12), (48, 40), (8, 200), (2, 400)])
+@pytest.mark.parametrize("n_seqs,length", [(256, 1), (256, 3), (64, 12), (48, 40), (8, 200), (2, 400)])
 def test_auto_runs_the_reported_path(n_seqs, length):
     """chunk = 0 at the benchmark's heads: bitwise the path the library
     reports, and within that path's oracle bars."""
@@ -220,4 +220,63 @@ def test_neumann_gated():
                                         x["dt_bias"], x["cu_seqlens"], x["initial_state"])
     eo, es = rel_l2(o.cpu(), o_ref), rel_l2(sT.cpu(), s_ref)
     _log("neumann_gated", o=eo, state=es)
+    assert eo <= O_BAR and es <= STATE_BAR
+
+
+# ------------------------------------------------------------ single-wave carry
+def _short_lengths(C):
+    """Ragged lengths whose average fits in one chunk (the single-wave carry
+    runs), with an empty sequence and sequences of one, several and C tokens
+    and one of more than two chunks."""
+    return (1, 5, C, 2 * C + 3, 0, 7, 9, 11, 13, 2, C - 1, 3)
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("chunk", [16, 32, 64])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_wave_carry_shapes(d, chunk, dtype):
+    dev = require_gpu()
+    lengths = _short_lengths(chunk)
+    assert sum(lengths) <= len(lengths) * chunk
+    x = _case(lengths, d=d, dtype=dtype, g_mu=-4.0, seed=100 + d + chunk)
+    o, sT = _run(x, dev, chunk)
+    o_ref, s_ref = _oracle(x)
+    eo, es = rel_l2(o, o_ref), rel_l2(sT, s_ref)
+    _log("wave_carry_d%d_C%d_%s" % (d, chunk, dtype), o=eo, state=es)
+    assert torch.isfinite(o.float()).all() and torch.isfinite(sT).all()
+    assert eo <= O_BAR and es <= STATE_BAR
+
+
+def test_wave_carry_benchmark_heads_no_state():
+    """The benchmark's heads, 128 sequences of 16 tokens, zero initial state
+    (the shape of the bench's short-sequence batch)."""
+    dev = require_gpu()
+    x = _case((16,) * 128, hqk=16, hv=32, d=128, state_std=0.0, seed=110)
+    o, sT = _run(x, dev, 16)
+    rng = np.random.default_rng(7)
+    for n in rng.choice(128, size=6, replace=False):
+        h = int(rng.integers(0, 32))
+        c = chain_slice(x, int(n), h)
+        o_ref, s_ref = oracle.prefill(c["q"], c["k"], c["v"], c["g"], c["beta"],
+                                      c["cu_seqlens"], c["initial_state"])
+        cu = x["cu_seqlens"].numpy()
+        eo = rel_l2(o[int(cu[n]):int(cu[n + 1]), h:h + 1], o_ref)
+        es = rel_l2(sT[n:n + 1, h:h + 1], s_ref)
+        assert eo <= O_BAR and es <= STATE_BAR, (n, h, eo, es)
+    _log("wave_carry_N128_L16", o=eo, state=es)
+
+
+def test_wave_carry_alias_and_gated():
+    dev = require_gpu()
+    x = _case(_short_lengths(32), d=64, raw_gate=True, seed=111)
+    dd = to_dev(x, dev)
+    fs = dd["initial_state"].clone()
+    o, sT = gdn.prefill_gated(dd["q"], dd["k"], dd["v"], dd["a"], dd["b"], dd["A_log"],
+                              dd["dt_bias"], dd["cu_seqlens"], initial_state=fs, chunk=32,
+                              final_state=fs)
+    torch.cuda.synchronize()
+    o_ref, s_ref = oracle.prefill_gated(x["q"], x["k"], x["v"], x["a"], x["b"], x["A_log"],
+                                        x["dt_bias"], x["cu_seqlens"], x["initial_state"])
+    eo, es = rel_l2(o.cpu(), o_ref), rel_l2(sT.cpu(), s_ref)
+    _log("wave_carry_gated_in_place", o=eo, state=es)
     assert eo <= O_BAR and es <= STATE_BAR
