@@ -1154,6 +1154,32 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
         Y[ib][e] = BufElem<TIn>::load1(rv, (uint32_t)((16 * ib + 4 * g4 + e) * hv * D + l16));
     }
     const float glast = dec[C - 1];
+    // At C = 32 the T', P and Q operands of the whole chunk are loaded here
+    // too, so that the chunk waits for memory once (64 x 32 tokens: 74.8 ->
+    // 69.3 us). At C = 16 the extra registers cost more occupancy than the
+    // wait (512 x 12 tokens: 314.8 -> 371.6 us), and at C = 64 they would not
+    // fit; there the operands are loaded where they are used.
+    constexpr bool PRELOAD = C == 32;
+    const rsrc_t rq = make_rsrc(q + (t0 * hqk + hk) * D, (uint32_t)(nv * hqk * D * sizeof(TIn)));
+    uint4 ta[PRELOAD ? NIB * KS : 1], pa[PRELOAD ? NIB * KS : 1];
+    uint2 qa[PRELOAD ? NIB * DS * 2 : 1];
+    if constexpr (PRELOAD) {
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+        for (int st = 0; st < frag_steps<C>(ib); ++st) {
+          const uint32_t off = (uint32_t)(((ib * KS + st) * 64 + lane) * 16);
+          ta[ib * KS + st] = buf_load_b128(rt, off);
+          pa[ib * KS + st] = buf_load_b128(rp, off);
+        }
+#pragma unroll
+        for (int st = 0; st < DS; ++st) {
+          const uint32_t e0 = (uint32_t)((16 * ib + l16) * hqk * D + 32 * st + 4 * g4);
+          qa[(ib * DS + st) * 2] = BufElem<TIn>::load4_bf16(rq, e0);
+          qa[(ib * DS + st) * 2 + 1] = BufElem<TIn>::load4_bf16(rq, e0 + 16);
+        }
+      }
+    }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // K has landed in LDS
 
     // ---- the state as the bf16 B operand of S^T, key order as above
@@ -1186,28 +1212,35 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
       U[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < frag_steps<C>(ib); ++st) {
-        const uint4 a = buf_load_b128(rt, (uint32_t)(((ib * KS + st) * 64 + lane) * 16));
+        const uint4 a = PRELOAD ? ta[(ib * KS + st) % (PRELOAD ? NIB * KS : 1)]
+                                : buf_load_b128(rt, (uint32_t)(((ib * KS + st) * 64 + lane) * 16));
         U[ib] = mfma_16x16x32(a, u_operand<NIB>(Y, st, nullptr), U[ib]);
       }
     }
 
     // ---- O = exp(gamma) (Q S^T) + P U, stored by block
-    const rsrc_t rq = make_rsrc(q + (t0 * hqk + hk) * D, (uint32_t)(nv * hqk * D * sizeof(TIn)));
     const rsrc_t ro = make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * sizeof(TIn)));
 #pragma unroll
     for (int ib = 0; ib < NIB; ++ib) {
       f32x4 qs = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < DS; ++st) {
-        const uint32_t e0 = (uint32_t)((16 * ib + l16) * hqk * D + 32 * st + 4 * g4);
-        qs = mfma_16x16x32(key_operand(BufElem<TIn>::load4_bf16(rq, e0),
-                                       BufElem<TIn>::load4_bf16(rq, e0 + 16)),
-                           SB[st], qs);
+        uint2 lo, hi;
+        if constexpr (PRELOAD) {
+          lo = qa[((ib * DS + st) * 2) % (PRELOAD ? NIB * DS * 2 : 1)];
+          hi = qa[((ib * DS + st) * 2 + 1) % (PRELOAD ? NIB * DS * 2 : 1)];
+        } else {
+          const uint32_t e0 = (uint32_t)((16 * ib + l16) * hqk * D + 32 * st + 4 * g4);
+          lo = BufElem<TIn>::load4_bf16(rq, e0);
+          hi = BufElem<TIn>::load4_bf16(rq, e0 + 16);
+        }
+        qs = mfma_16x16x32(key_operand(lo, hi), SB[st], qs);
       }
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < frag_steps<C>(ib); ++st) {
-        const uint4 a = buf_load_b128(rp, (uint32_t)(((ib * KS + st) * 64 + lane) * 16));
+        const uint4 a = PRELOAD ? pa[(ib * KS + st) % (PRELOAD ? NIB * KS : 1)]
+                                : buf_load_b128(rp, (uint32_t)(((ib * KS + st) * 64 + lane) * 16));
         acc = mfma_16x16x32(a, u_operand<NIB>(U, st, nullptr), acc);
       }
 #pragma unroll
