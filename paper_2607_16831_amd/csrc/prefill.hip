@@ -1120,9 +1120,6 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
   const bool kcopied = sizeof(TIn) != 2;
   const uint16_t *ksrc = kcopied ? kcopy : reinterpret_cast<const uint16_t *>(k);
   const int kstride = kcopied ? D : hqk * D;
-  uint32_t koff[WC::NKI];
-#pragma unroll
-  for (int m = 0; m < WC::NKI; ++m) koff[m] = copy_offset<D, C, TIn>(m, lane, kstride, hv);
 
   for (int lc = 0; lc < nch; ++lc) {
     const int64_t t0 = seq_t0 + (int64_t)lc * C;
@@ -1135,7 +1132,7 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
     for (int m = 0; m < WC::NKI; ++m) {
       // (the offset goes in as a plain scalar: with an array element as the
       // builtin's argument the host pass emitted no launch stub)
-      const uint32_t off = koff[m];
+      const uint32_t off = copy_offset<D, C, TIn>(m, lane, kstride, hv);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void *)(K + 512 * m), 16, off, 0, 0, 0);
     }
     const rsrc_t rt = make_rsrc(tfrag + slot * F::FRAG, F::FRAG * 2);
@@ -1194,6 +1191,7 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
     // ---- Y = V - exp(gamma) (K S^T), block by block
 #pragma unroll
     for (int ib = 0; ib < NIB; ++ib) {
+      if (!PRELOAD) asm volatile("" ::: "memory");  // operands read per block
       f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < DS; ++st) {
@@ -1222,6 +1220,9 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
     const rsrc_t ro = make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * sizeof(TIn)));
 #pragma unroll
     for (int ib = 0; ib < NIB; ++ib) {
+      // without preloading, keep each block's loads in its own iteration
+      // (hoisted, the loads of all blocks held twice the registers)
+      if (!PRELOAD) asm volatile("" ::: "memory");
       f32x4 qs = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < DS; ++st) {
@@ -1255,6 +1256,7 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
     for (int st = 0; st < KS; ++st) bu[st] = u_operand<NIB>(U, st, he);
 #pragma unroll
     for (int t = 0; t < NKT; ++t) {
+      if (!PRELOAD) asm volatile("" ::: "memory");  // K^T operands read per tile
       f32x4 acc = Sacc[t] * glast;
 #pragma unroll
       for (int st = 0; st < KS; ++st) acc = mfma_16x16x32(kt_operand<D>(K, t, st, l16, g4), bu[st], acc);
