@@ -1083,7 +1083,6 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
     int n_units, int hqk, int hv, int group) {
   using F = Cfg<D, C>;
   using WC = WaveCfg<D, C>;
-  using CC = CarryCfg<D, C, TIn>;
   constexpr int NIB = F::NIB, KS = F::KS, DS = F::DS, NKT = F::NKT, NVT = F::NVT;
   __shared__ __attribute__((aligned(16))) uint16_t Kw[WC::WAVES][F::CP * D];
 
