@@ -104,6 +104,8 @@ typedef __attribute__((address_space(3))) void lds_void;
 //   T[b][c] = -(sum_{m=c+1..b} T[b][m] A[m][c]) T[c][c]^-1    (c < b),
 // carried in transposed form so that every intermediate stays in the
 // accumulator layout of the fp32 16x16x4 matrix instruction.
+constexpr int kGateHeads = 8;  // gates staged in LDS per chunk-local work-group
+
 template <int D, int C>
 struct LocalLds {
   static constexpr int NIB = C / 16;
@@ -118,6 +120,9 @@ struct LocalLds {
       float bet[4][64];
     } inv;
   } u;
+  // g and beta of the first kGateHeads value heads of the group, lane t
+  // holding token t
+  float gate_g[kGateHeads][64], gate_b[kGateHeads][64];
 };
 
 // Block rows of row set p (one row set per pair of wavefronts): the longest
@@ -223,25 +228,34 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   const rsrc_t rk = make_rsrc(k + (t0 * hqk + hk) * D, rowb);
   const rsrc_t rq = make_rsrc(q + (t0 * hqk + hk) * D, rowb);
   // g and beta of token `lane` for value head hh (0 past the end), read or
-  // formed from the raw gate inputs
-  auto load_gates = [&](int hh, float &gl_, float &bta_) {
-    if (gate.a_log != nullptr) {  // uniform over the launch
-      const rsrc_t ra = make_rsrc(gate.a + t0 * hv, (uint32_t)(nvalid * hv * 4));
-      const rsrc_t rb = make_rsrc(gate.b + t0 * hv, (uint32_t)(nvalid * hv * 4));
-      const float ga = buf_load_f32(ra, (uint32_t)(lane * hv + hh) * 4u);
-      const float gb = buf_load_f32(rb, (uint32_t)(lane * hv + hh) * 4u);
+  // formed from the raw gate inputs: the loads first, the arithmetic once
+  // they have landed.
+  const bool raw_gates = gate.a_log != nullptr;  // uniform over the launch
+  const rsrc_t rga = make_rsrc((raw_gates ? gate.a : g) + t0 * hv, (uint32_t)(nvalid * hv * 4));
+  const rsrc_t rgb = make_rsrc((raw_gates ? gate.b : beta) + t0 * hv, (uint32_t)(nvalid * hv * 4));
+  auto gate_loads = [&](int hh, float &x, float &y) {
+    x = buf_load_f32(rga, (uint32_t)(lane * hv + hh) * 4u);
+    y = buf_load_f32(rgb, (uint32_t)(lane * hv + hh) * 4u);
+  };
+  auto gate_values = [&](int hh, float x, float y, float &gl_, float &bta_) {
+    if (raw_gates) {
       const bool in = lane < nvalid;
-      gl_ = in ? gate_log_decay(ga, gate.a_log[hh], gate.dt_bias[hh]) : 0.f;
-      bta_ = in ? gate_beta(gb) : 0.f;
+      gl_ = in ? gate_log_decay(x, gate.a_log[hh], gate.dt_bias[hh]) : 0.f;
+      bta_ = in ? gate_beta(y) : 0.f;
     } else {
-      const rsrc_t rg = make_rsrc(g + t0 * hv, (uint32_t)(nvalid * hv * 4));
-      const rsrc_t rb = make_rsrc(beta + t0 * hv, (uint32_t)(nvalid * hv * 4));
-      gl_ = buf_load_f32(rg, (uint32_t)(lane * hv + hh) * 4u);
-      bta_ = buf_load_f32(rb, (uint32_t)(lane * hv + hh) * 4u);
+      gl_ = x;
+      bta_ = y;
     }
   };
-  float gl, bta;
-  load_gates(hk * group, gl, bta);
+  // Gates of the group's heads, read with the tiles; a head past the first
+  // kGateHeads reads its own in the loop below.
+  float gxv[kGateHeads], gyv[kGateHeads];
+#pragma unroll
+  for (int i = 0; i < kGateHeads; ++i) {
+    gxv[i] = 0.f;
+    gyv[i] = 0.f;
+    if (i < group) gate_loads(hk * group + i, gxv[i], gyv[i]);
+  }
   if constexpr (sizeof(TIn) == 2) {
     // Buffer-to-LDS copies: lane i of a copy fills bytes [16 i, 16 i + 16) of
     // its 1 KB piece, so the source offset picks the global 16-byte piece that
@@ -280,6 +294,12 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (wave == 0) {
+#pragma unroll
+    for (int i = 0; i < kGateHeads; ++i) {
+      if (i < group) gate_values(hk * group + i, gxv[i], gyv[i], L.gate_g[i][lane], L.gate_b[i][lane]);
+    }
+  }
   __syncthreads();
 
   // ---- Q of this chunk for the carry, in the A-operand order of Q S^T:
@@ -331,9 +351,17 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   for (int gi = 0; gi < group; ++gi) {
     const int h = hk * group + gi;
     const int64_t slot = (int64_t)cidx * hv + h;
-    // the next head's gates are read while this one is formed
-    float gl_next = 0.f, bta_next = 0.f;
-    if (gi + 1 < group) load_gates(h + 1, gl_next, bta_next);
+    // From LDS: a loop-carried value loaded from global memory would make
+    // every iteration wait for all earlier stores as well.
+    float gl, bta;
+    if (gi < kGateHeads) {
+      gl = L.gate_g[gi][lane];
+      bta = L.gate_b[gi][lane];
+    } else {
+      float x, y;
+      gate_loads(h, x, y);
+      gate_values(h, x, y, gl, bta);
+    }
     // gamma: inclusive prefix sum of g over the chunk, lane t holding token t
     // (lanes past the end and past C hold g = 0: they repeat the last value).
     const float gam = wave_prefix_sum(gl);
@@ -349,23 +377,24 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     gw[lane] = gam;
     bw[lane] = bta;
     wave_lds_fence();
-  #pragma unroll
+#pragma unroll
     for (int r = 0; r < 2; ++r) {
       const int ib = rows[r];
       if (ib < 0) continue;
       const int i = 16 * ib + l16;
       const float gami = gw[i], bi = bw[i];
       f32x4 Pt[NIB];
-  #pragma unroll
+#pragma unroll
       for (int jb = 0; jb < NIB; ++jb) {
         Pt[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
         if (jb > ib) continue;
         const float4 gj = *reinterpret_cast<const float4 *>(&gw[16 * jb + 4 * g4]);
         const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
-  #pragma unroll
+#pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int j = 16 * jb + 4 * g4 + e;
-          const float dec = (j <= i) ? __expf(gami - gjv[e]) : 0.f;
+          // exp(-inf) = 0 above the diagonal; a select, not a branch
+          const float dec = __expf((j <= i) ? gami - gjv[e] : -INFINITY);
           Pt[jb][e] = prod ? dec * G[r][jb][e] : ((j < i) ? bi * dec * G[r][jb][e] : 0.f);
         }
         if (!prod)
@@ -376,7 +405,7 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
         // P as A-operand fragments: step s takes tile 2s (elements 0-3) and
         // tile 2s+1 (elements 4-7), i.e. the token order of tok_pos().
         uint16_t *pf = pfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
-  #pragma unroll
+#pragma unroll
         for (int s = 0; s < KS; ++s) {
           if (2 * s > ib) continue;  // above the diagonal: zero, never stored or read
           const f32x4 lo4 = Pt[2 * s];
@@ -393,7 +422,7 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     // stores it transposed (linv[b] row c = column c of the inverse).
     if (NEUMANN && wave < NIB) {
       const f32x4 tb = neumann_diag<AP>(L.u.inv.A[wave * (wave + 1) / 2 + wave], g4, l16);
-  #pragma unroll
+#pragma unroll
       for (int e = 0; e < 4; ++e) L.u.inv.linv[wave][l16 * 17 + 4 * g4 + e] = tb[e];
     }
     // Forward substitution: lane (b, c) = (g4, l16) solves (I + A[b][b]) x =
@@ -403,10 +432,10 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
       const int b = min(g4, NIB - 1);  // lanes past the last block repeat it
       const float *Ab = L.u.inv.A[b * (b + 1) / 2 + b];
       float x[16];
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < 16; ++i) {
         float s0 = (i == l16) ? 1.f : 0.f, s1 = 0.f;
-  #pragma unroll
+#pragma unroll
         for (int j = 0; j + 1 < i; j += 2) {
           s0 -= Ab[i * AP + j] * x[j];
           s1 -= Ab[i * AP + j + 1] * x[j + 1];
@@ -415,7 +444,7 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
         x[i] = s0 + s1;
       }
       if (g4 < NIB) {
-  #pragma unroll
+#pragma unroll
         for (int i = 0; i < 16; ++i) L.u.inv.linv[b][l16 * 17 + i] = x[i];
       }
     }
@@ -425,35 +454,35 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     if (wave < NIB) {
       const int ib = wave;
       f32x4 Z[NIB];
-  #pragma unroll
+#pragma unroll
       for (int c = 0; c < NIB; ++c) {
         Z[c] = f32x4{0.f, 0.f, 0.f, 0.f};
         if (c == ib) {
-  #pragma unroll
+#pragma unroll
           for (int e = 0; e < 4; ++e) Z[c][e] = L.u.inv.linv[ib][(4 * g4 + e) * 17 + l16];
         }
       }
-  #pragma unroll
+#pragma unroll
       for (int c = NIB - 2; c >= 0; --c) {
         if (c >= ib) continue;
         f32x4 R = f32x4{0.f, 0.f, 0.f, 0.f};
-  #pragma unroll
+#pragma unroll
         for (int m = 1; m < NIB; ++m) {
           if (m <= c || m > ib) continue;
           const float *Amc = L.u.inv.A[m * (m + 1) / 2 + c];
-  #pragma unroll
+#pragma unroll
           for (int kk = 0; kk < 4; ++kk)
             R = mfma_16x16x4_f32(Amc[(4 * g4 + kk) * AP + l16], Z[m][kk], R);
         }
         f32x4 Zc = f32x4{0.f, 0.f, 0.f, 0.f};
-  #pragma unroll
+#pragma unroll
         for (int kk = 0; kk < 4; ++kk)
           Zc = mfma_16x16x4_f32(L.u.inv.linv[c][l16 * 17 + 4 * g4 + kk], R[kk], Zc);
         Z[c] = -Zc;
       }
       // Fold beta into the factor: the carry uses T' = T diag(beta), so that
       // U = T' (V - exp(gamma) X) needs no beta of its own.
-  #pragma unroll
+#pragma unroll
       for (int c = 0; c < NIB; ++c) {
         if (c > ib) continue;
         const float4 bc = *reinterpret_cast<const float4 *>(&bw[16 * c + 4 * g4]);
@@ -464,7 +493,7 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
       }
       // T' as A-operand fragments, same token order as P.
       uint16_t *tf = tfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
-  #pragma unroll
+#pragma unroll
       for (int s = 0; s < KS; ++s) {
         if (2 * s > ib) continue;  // above the diagonal: zero, never stored or read
         const f32x4 lo4 = Z[2 * s];
@@ -475,8 +504,6 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
       }
     }
     lds_barrier();  // the next head rewrites A, the inverses and the gate copies
-    gl = gl_next;
-    bta = bta_next;
   }  // value heads of the group
 }
 
