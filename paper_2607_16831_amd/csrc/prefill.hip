@@ -86,11 +86,12 @@ __device__ __forceinline__ int kn_index(int row, int col) {
 typedef __attribute__((address_space(3))) void lds_void;
 
 // ============================================================ chunk-local
-// One work-group per (chunk, key head): K K^T and K Q^T once, then for each
-// value head of the GQA group in turn gamma, A, P and T = (I + A)^-1, written
-// as bf16 A-operand fragments. The Gram products depend only on the key
-// head, so the heads of a group share one K and Q tile and one pair of
-// products; only the decay masks, the solve and the stores repeat per head.
+// One work-group per (chunk, value head): gamma, K K^T and K Q^T, then A, P
+// and T = (I + A)^-1, written as bf16 A-operand fragments. The two Gram
+// products depend only on the key head; the value heads of a GQA group each
+// recompute them (a few dozen matrix instructions) rather than share a
+// longer work-group, and the launch order puts the heads of one group on
+// the same XCD so that the second reads K and Q from its L2.
 //
 // The 16x16 tiles of the two lower-triangular Gram products are dealt out
 // evenly: wavefront w computes product (w & 1) (0: K K^T for A, 1: K Q^T
@@ -104,8 +105,6 @@ typedef __attribute__((address_space(3))) void lds_void;
 //   T[b][c] = -(sum_{m=c+1..b} T[b][m] A[m][c]) T[c][c]^-1    (c < b),
 // carried in transposed form so that every intermediate stays in the
 // accumulator layout of the fp32 16x16x4 matrix instruction.
-constexpr int kGateHeads = 8;  // gates staged in LDS per chunk-local work-group
-
 template <int D, int C>
 struct LocalLds {
   static constexpr int NIB = C / 16;
@@ -120,9 +119,6 @@ struct LocalLds {
       float bet[4][64];
     } inv;
   } u;
-  // g and beta of the first kGateHeads value heads of the group, lane t
-  // holding token t
-  float gate_g[kGateHeads][64], gate_b[kGateHeads][64];
 };
 
 // Block rows of row set p (one row set per pair of wavefronts): the longest
@@ -188,10 +184,17 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   __shared__ __attribute__((aligned(16))) LL L;
   uint16_t *Kt = L.u.kq, *Qt = L.u.kq + C * D;
 
-  // Block id -> (chunk, key head) pair.
-  const int pair = blockIdx.x;
+  // Block id -> (chunk, key head) pair and head of the group. Work-groups are
+  // dealt to the eight XCDs round robin, so ids b and b + 8 share one: the
+  // heads of a group for one pair take ids 8 (group j + gi) + x.
+  const int bid = blockIdx.x;
+  const int xg = bid & 7, jj = bid >> 3;
+  const int gi = jj % group;
+  const int pair = (jj / group) * 8 + xg;
   if (pair >= n_pairs) return;
   const int cidx = pair / hqk, hk = pair - cidx * hqk;
+  const int h = hk * group + gi;
+  const int64_t slot = (int64_t)cidx * hv + h;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
@@ -227,34 +230,22 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   const uint32_t rowb = (uint32_t)(nvalid * hqk * D * sizeof(TIn));
   const rsrc_t rk = make_rsrc(k + (t0 * hqk + hk) * D, rowb);
   const rsrc_t rq = make_rsrc(q + (t0 * hqk + hk) * D, rowb);
-  // g and beta of token `lane` for value head hh (0 past the end), read or
-  // formed from the raw gate inputs: the loads first, the arithmetic once
-  // they have landed.
-  const bool raw_gates = gate.a_log != nullptr;  // uniform over the launch
-  const rsrc_t rga = make_rsrc((raw_gates ? gate.a : g) + t0 * hv, (uint32_t)(nvalid * hv * 4));
-  const rsrc_t rgb = make_rsrc((raw_gates ? gate.b : beta) + t0 * hv, (uint32_t)(nvalid * hv * 4));
-  auto gate_loads = [&](int hh, float &x, float &y) {
-    x = buf_load_f32(rga, (uint32_t)(lane * hv + hh) * 4u);
-    y = buf_load_f32(rgb, (uint32_t)(lane * hv + hh) * 4u);
-  };
-  auto gate_values = [&](int hh, float x, float y, float &gl_, float &bta_) {
-    if (raw_gates) {
-      const bool in = lane < nvalid;
-      gl_ = in ? gate_log_decay(x, gate.a_log[hh], gate.dt_bias[hh]) : 0.f;
-      bta_ = in ? gate_beta(y) : 0.f;
-    } else {
-      gl_ = x;
-      bta_ = y;
-    }
-  };
-  // Gates of the group's heads, read with the tiles; a head past the first
-  // kGateHeads reads its own in the loop below.
-  float gxv[kGateHeads], gyv[kGateHeads];
-#pragma unroll
-  for (int i = 0; i < kGateHeads; ++i) {
-    gxv[i] = 0.f;
-    gyv[i] = 0.f;
-    if (i < group) gate_loads(hk * group + i, gxv[i], gyv[i]);
+  // g and beta of token `lane` (0 past the end), read or formed from the raw
+  // gate inputs
+  float gl, bta;
+  if (gate.a_log != nullptr) {  // uniform over the launch
+    const rsrc_t ra = make_rsrc(gate.a + t0 * hv, (uint32_t)(nvalid * hv * 4));
+    const rsrc_t rb = make_rsrc(gate.b + t0 * hv, (uint32_t)(nvalid * hv * 4));
+    const float ga = buf_load_f32(ra, (uint32_t)(lane * hv + h) * 4u);
+    const float gb = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
+    const bool in = lane < nvalid;
+    gl = in ? gate_log_decay(ga, gate.a_log[h], gate.dt_bias[h]) : 0.f;
+    bta = in ? gate_beta(gb) : 0.f;
+  } else {
+    const rsrc_t rg = make_rsrc(g + t0 * hv, (uint32_t)(nvalid * hv * 4));
+    const rsrc_t rb = make_rsrc(beta + t0 * hv, (uint32_t)(nvalid * hv * 4));
+    gl = buf_load_f32(rg, (uint32_t)(lane * hv + h) * 4u);
+    bta = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
   }
   if constexpr (sizeof(TIn) == 2) {
     // Buffer-to-LDS copies: lane i of a copy fills bytes [16 i, 16 i + 16) of
@@ -293,19 +284,23 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
       }
     }
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  if (wave == 0) {
-#pragma unroll
-    for (int i = 0; i < kGateHeads; ++i) {
-      if (i < group) gate_values(hk * group + i, gxv[i], gyv[i], L.gate_g[i][lane], L.gate_b[i][lane]);
-    }
+  // gamma: inclusive prefix sum of g over the chunk, lane t holding token t
+  // (lanes past the end and past C hold g = 0: they repeat the last value).
+  const float gam = wave_prefix_sum(gl);
+  if (wave == 0 && lane < C) {
+    // decay factors for the carry: exp(gamma_i) and exp(gamma_last - gamma_i)
+    const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gam), C - 1));
+    dec_ws[slot * 2 * C + lane] = __expf(gam);
+    dec_ws[slot * 2 * C + C + lane] = __expf(glast - gam);
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
   // ---- Q of this chunk for the carry, in the A-operand order of Q S^T:
   // block ib, step s, lane (l16, g4) holds Q[16 ib + l16][32 s + 8 g4 + (0..7)].
   // For f32 inputs also a bf16 copy of K, row-major [C][D], for the carry.
-  if (wave < NIB) {
+  // One value head of the group writes them.
+  if (gi == 0 && wave < NIB) {
     const int64_t base = ((int64_t)cidx * hqk + hk) * (C * D);
     uint16_t *qf = qfrag + base + ((int64_t)wave * F::DS * 64 + lane) * 8;
 #pragma unroll
@@ -348,163 +343,136 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   }
   lds_barrier();  // the K and Q tiles are dead; the space is reused below
 
-  for (int gi = 0; gi < group; ++gi) {
-    const int h = hk * group + gi;
-    const int64_t slot = (int64_t)cidx * hv + h;
-    // From LDS: a loop-carried value loaded from global memory would make
-    // every iteration wait for all earlier stores as well.
-    float gl, bta;
-    if (gi < kGateHeads) {
-      gl = L.gate_g[gi][lane];
-      bta = L.gate_b[gi][lane];
-    } else {
-      float x, y;
-      gate_loads(h, x, y);
-      gate_values(h, x, y, gl, bta);
+  // ---- decay masks: A (product 0) to LDS, P (product 1) to global.
+  float *gw = L.u.inv.gam[wave], *bw = L.u.inv.bet[wave];
+  gw[lane] = gam;
+  bw[lane] = bta;
+  wave_lds_fence();
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int ib = rows[r];
+    if (ib < 0) continue;
+    const int i = 16 * ib + l16;
+    const float gami = gw[i], bi = bw[i];
+    f32x4 Pt[NIB];
+#pragma unroll
+    for (int jb = 0; jb < NIB; ++jb) {
+      Pt[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (jb > ib) continue;
+      const float4 gj = *reinterpret_cast<const float4 *>(&gw[16 * jb + 4 * g4]);
+      const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j = 16 * jb + 4 * g4 + e;
+        const float dec = (j <= i) ? __expf(gami - gjv[e]) : 0.f;
+        Pt[jb][e] = prod ? dec * G[r][jb][e] : ((j < i) ? bi * dec * G[r][jb][e] : 0.f);
+      }
+      if (!prod)
+        *reinterpret_cast<float4 *>(&L.u.inv.A[ib * (ib + 1) / 2 + jb][l16 * AP + 4 * g4]) =
+            make_float4(Pt[jb][0], Pt[jb][1], Pt[jb][2], Pt[jb][3]);
     }
-    // gamma: inclusive prefix sum of g over the chunk, lane t holding token t
-    // (lanes past the end and past C hold g = 0: they repeat the last value).
-    const float gam = wave_prefix_sum(gl);
-    if (wave == 0 && lane < C) {
-      // decay factors for the carry: exp(gamma_i) and exp(gamma_last - gamma_i)
-      const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gam), C - 1));
-      dec_ws[slot * 2 * C + lane] = __expf(gam);
-      dec_ws[slot * 2 * C + C + lane] = __expf(glast - gam);
-    }
-
-    // ---- decay masks: A (product 0) to LDS, P (product 1) to global.
-    float *gw = L.u.inv.gam[wave], *bw = L.u.inv.bet[wave];
-    gw[lane] = gam;
-    bw[lane] = bta;
-    wave_lds_fence();
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const int ib = rows[r];
-      if (ib < 0) continue;
-      const int i = 16 * ib + l16;
-      const float gami = gw[i], bi = bw[i];
-      f32x4 Pt[NIB];
-#pragma unroll
-      for (int jb = 0; jb < NIB; ++jb) {
-        Pt[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (jb > ib) continue;
-        const float4 gj = *reinterpret_cast<const float4 *>(&gw[16 * jb + 4 * g4]);
-        const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int j = 16 * jb + 4 * g4 + e;
-          // exp(-inf) = 0 above the diagonal; a select, not a branch
-          const float dec = __expf((j <= i) ? gami - gjv[e] : -INFINITY);
-          Pt[jb][e] = prod ? dec * G[r][jb][e] : ((j < i) ? bi * dec * G[r][jb][e] : 0.f);
-        }
-        if (!prod)
-          *reinterpret_cast<float4 *>(&L.u.inv.A[ib * (ib + 1) / 2 + jb][l16 * AP + 4 * g4]) =
-              make_float4(Pt[jb][0], Pt[jb][1], Pt[jb][2], Pt[jb][3]);
-      }
-      if (prod) {
-        // P as A-operand fragments: step s takes tile 2s (elements 0-3) and
-        // tile 2s+1 (elements 4-7), i.e. the token order of tok_pos().
-        uint16_t *pf = pfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          if (2 * s > ib) continue;  // above the diagonal: zero, never stored or read
-          const f32x4 lo4 = Pt[2 * s];
-          const f32x4 hi4 = (2 * s + 1 < NIB) ? Pt[(2 * s + 1) % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
-          *reinterpret_cast<uint4 *>(pf + s * 512) =
-              make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
-                         pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
-        }
-      }
-    }
-    lds_barrier();
-
-    // ---- diagonal blocks. Neumann product: wavefront b inverts block b and
-    // stores it transposed (linv[b] row c = column c of the inverse).
-    if (NEUMANN && wave < NIB) {
-      const f32x4 tb = neumann_diag<AP>(L.u.inv.A[wave * (wave + 1) / 2 + wave], g4, l16);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) L.u.inv.linv[wave][l16 * 17 + 4 * g4 + e] = tb[e];
-    }
-    // Forward substitution: lane (b, c) = (g4, l16) solves (I + A[b][b]) x =
-    // e_c, i.e. column c of T[b][b], and stores it as row c of the transposed
-    // inverse.
-    if (!NEUMANN && wave == 0) {
-      const int b = min(g4, NIB - 1);  // lanes past the last block repeat it
-      const float *Ab = L.u.inv.A[b * (b + 1) / 2 + b];
-      float x[16];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float s0 = (i == l16) ? 1.f : 0.f, s1 = 0.f;
-#pragma unroll
-        for (int j = 0; j + 1 < i; j += 2) {
-          s0 -= Ab[i * AP + j] * x[j];
-          s1 -= Ab[i * AP + j + 1] * x[j + 1];
-        }
-        if (i & 1) s0 -= Ab[i * AP + i - 1] * x[i - 1];
-        x[i] = s0 + s1;
-      }
-      if (g4 < NIB) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) L.u.inv.linv[b][l16 * 17 + i] = x[i];
-      }
-    }
-    lds_barrier();
-
-    // ---- block row ib = wave, right to left: Z[c] = (T[ib][c])^T.
-    if (wave < NIB) {
-      const int ib = wave;
-      f32x4 Z[NIB];
-#pragma unroll
-      for (int c = 0; c < NIB; ++c) {
-        Z[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (c == ib) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) Z[c][e] = L.u.inv.linv[ib][(4 * g4 + e) * 17 + l16];
-        }
-      }
-#pragma unroll
-      for (int c = NIB - 2; c >= 0; --c) {
-        if (c >= ib) continue;
-        f32x4 R = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int m = 1; m < NIB; ++m) {
-          if (m <= c || m > ib) continue;
-          const float *Amc = L.u.inv.A[m * (m + 1) / 2 + c];
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk)
-            R = mfma_16x16x4_f32(Amc[(4 * g4 + kk) * AP + l16], Z[m][kk], R);
-        }
-        f32x4 Zc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-          Zc = mfma_16x16x4_f32(L.u.inv.linv[c][l16 * 17 + 4 * g4 + kk], R[kk], Zc);
-        Z[c] = -Zc;
-      }
-      // Fold beta into the factor: the carry uses T' = T diag(beta), so that
-      // U = T' (V - exp(gamma) X) needs no beta of its own.
-#pragma unroll
-      for (int c = 0; c < NIB; ++c) {
-        if (c > ib) continue;
-        const float4 bc = *reinterpret_cast<const float4 *>(&bw[16 * c + 4 * g4]);
-        Z[c][0] *= bc.x;
-        Z[c][1] *= bc.y;
-        Z[c][2] *= bc.z;
-        Z[c][3] *= bc.w;
-      }
-      // T' as A-operand fragments, same token order as P.
-      uint16_t *tf = tfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
+    if (prod) {
+      // P as A-operand fragments: step s takes tile 2s (elements 0-3) and
+      // tile 2s+1 (elements 4-7), i.e. the token order of tok_pos().
+      uint16_t *pf = pfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         if (2 * s > ib) continue;  // above the diagonal: zero, never stored or read
-        const f32x4 lo4 = Z[2 * s];
-        const f32x4 hi4 = (2 * s + 1 < NIB) ? Z[(2 * s + 1) % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
-        *reinterpret_cast<uint4 *>(tf + s * 512) =
+        const f32x4 lo4 = Pt[2 * s];
+        const f32x4 hi4 = (2 * s + 1 < NIB) ? Pt[(2 * s + 1) % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
+        *reinterpret_cast<uint4 *>(pf + s * 512) =
             make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
                        pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
       }
     }
-    lds_barrier();  // the next head rewrites A, the inverses and the gate copies
-  }  // value heads of the group
+  }
+  lds_barrier();
+
+  // ---- diagonal blocks. Neumann product: wavefront b inverts block b and
+  // stores it transposed (linv[b] row c = column c of the inverse).
+  if (NEUMANN && wave < NIB) {
+    const f32x4 tb = neumann_diag<AP>(L.u.inv.A[wave * (wave + 1) / 2 + wave], g4, l16);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) L.u.inv.linv[wave][l16 * 17 + 4 * g4 + e] = tb[e];
+  }
+  // Forward substitution: lane (b, c) = (g4, l16) solves (I + A[b][b]) x =
+  // e_c, i.e. column c of T[b][b], and stores it as row c of the transposed
+  // inverse.
+  if (!NEUMANN && wave == 0) {
+    const int b = min(g4, NIB - 1);  // lanes past the last block repeat it
+    const float *Ab = L.u.inv.A[b * (b + 1) / 2 + b];
+    float x[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      float s0 = (i == l16) ? 1.f : 0.f, s1 = 0.f;
+#pragma unroll
+      for (int j = 0; j + 1 < i; j += 2) {
+        s0 -= Ab[i * AP + j] * x[j];
+        s1 -= Ab[i * AP + j + 1] * x[j + 1];
+      }
+      if (i & 1) s0 -= Ab[i * AP + i - 1] * x[i - 1];
+      x[i] = s0 + s1;
+    }
+    if (g4 < NIB) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) L.u.inv.linv[b][l16 * 17 + i] = x[i];
+    }
+  }
+  lds_barrier();
+
+  // ---- block row ib = wave, right to left: Z[c] = (T[ib][c])^T.
+  if (wave < NIB) {
+    const int ib = wave;
+    f32x4 Z[NIB];
+#pragma unroll
+    for (int c = 0; c < NIB; ++c) {
+      Z[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (c == ib) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Z[c][e] = L.u.inv.linv[ib][(4 * g4 + e) * 17 + l16];
+      }
+    }
+#pragma unroll
+    for (int c = NIB - 2; c >= 0; --c) {
+      if (c >= ib) continue;
+      f32x4 R = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int m = 1; m < NIB; ++m) {
+        if (m <= c || m > ib) continue;
+        const float *Amc = L.u.inv.A[m * (m + 1) / 2 + c];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          R = mfma_16x16x4_f32(Amc[(4 * g4 + kk) * AP + l16], Z[m][kk], R);
+      }
+      f32x4 Zc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+        Zc = mfma_16x16x4_f32(L.u.inv.linv[c][l16 * 17 + 4 * g4 + kk], R[kk], Zc);
+      Z[c] = -Zc;
+    }
+    // Fold beta into the factor: the carry uses T' = T diag(beta), so that
+    // U = T' (V - exp(gamma) X) needs no beta of its own.
+#pragma unroll
+    for (int c = 0; c < NIB; ++c) {
+      if (c > ib) continue;
+      const float4 bc = *reinterpret_cast<const float4 *>(&bw[16 * c + 4 * g4]);
+      Z[c][0] *= bc.x;
+      Z[c][1] *= bc.y;
+      Z[c][2] *= bc.z;
+      Z[c][3] *= bc.w;
+    }
+    // T' as A-operand fragments, same token order as P.
+    uint16_t *tf = tfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      if (2 * s > ib) continue;  // above the diagonal: zero, never stored or read
+      const f32x4 lo4 = Z[2 * s];
+      const f32x4 hi4 = (2 * s + 1 < NIB) ? Z[(2 * s + 1) % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
+      *reinterpret_cast<uint4 *>(tf + s * 512) =
+          make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
+                     pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
+    }
+  }
 }
 
 // ============================================================ chunk carry
@@ -1110,6 +1078,7 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
     int n_units, int hqk, int hv, int group) {
   using F = Cfg<D, C>;
   using WC = WaveCfg<D, C>;
+  using CC = CarryCfg<D, C, TIn>;
   constexpr int NIB = F::NIB, KS = F::KS, DS = F::DS, NKT = F::NKT, NVT = F::NVT;
   __shared__ __attribute__((aligned(16))) uint16_t Kw[WC::WAVES][F::CP * D];
 
@@ -1336,9 +1305,9 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
 
   const int64_t nc = chunk_bound(a.n_seqs, a.n_tokens, C);
   if (a.n_tokens > 0) {
-    // one work-group per (chunk, key head) pair
+    // (chunk, key head) pairs in groups of eight, times the heads of a group.
     const int64_t pairs = nc * a.hqk;
-    const int64_t lblocks = pairs;
+    const int64_t lblocks = ((pairs + 7) / 8) * 8 * group;
     auto local = a.neumann ? chunk_local_kernel<D, C, TIn, true>
                            : chunk_local_kernel<D, C, TIn, false>;
     hipLaunchKernelGGL(local, dim3((unsigned)lblocks), dim3(256), 0, a.stream, (const TIn *)a.q, (const TIn *)a.k, a.g, a.beta, a.gate,
