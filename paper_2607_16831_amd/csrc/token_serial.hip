@@ -17,10 +17,11 @@
 // Launch shape as in the decode kernel: a state row of D fp32 values is held
 // by D/4 lanes, 16 bytes each; a wavefront holds PASSES such row groups of one
 // (sequence, value head) pair. The per-token inputs (k, q, the wavefront's v
-// entries) are fetched TB tokens ahead into registers, each slot refilled
-// right after it is consumed, and the gates of the next block of TB tokens in
-// one vector load; loads past the sequence end are clamped to its last token
-// and never used. Whole blocks run in the loop, the remaining tokens after it.
+// entries) are fetched TB tokens ahead into registers (TB = 1 when sequences
+// hold about one token), each slot refilled right after it is consumed, and
+// the gates of the next block of TB tokens in one vector load; loads past the
+// sequence end are clamped to its last token and never used. Whole blocks run
+// in the loop, the remaining tokens after it.
 #include "gdn_device.h"
 #include "gdn_launch.h"
 
@@ -208,9 +209,8 @@ __global__ __launch_bounds__(256) void token_serial_kernel(
   for (int p = 0; p < PASSES; ++p) store_stream(final_state + soff + (int64_t)p * RPP * D, s[p]);
 }
 
-template <int D, int PASSES, typename TIn>
+template <int D, int PASSES, int TB, typename TIn>
 static hipError_t launch_serial_p(const PrefillArgs &a, int64_t total_rows) {
-  constexpr int TB = 4;
   constexpr int RPW = (kWave / (D / 4)) * PASSES;
   const int64_t rows_per_block = RPW * 4;
   const int64_t blocks = (total_rows + rows_per_block - 1) / rows_per_block;
@@ -223,16 +223,29 @@ static hipError_t launch_serial_p(const PrefillArgs &a, int64_t total_rows) {
   return hipGetLastError();
 }
 
+template <int D, int PASSES, typename TIn>
+static hipError_t launch_serial_pb(const PrefillArgs &a, int64_t total_rows) {
+  // With at most one token per sequence on average, prefetching more tokens
+  // only costs registers (the loads past a sequence's end are clamped).
+  if (a.n_tokens <= a.n_seqs) return launch_serial_p<D, PASSES, 1, TIn>(a, total_rows);
+  return launch_serial_p<D, PASSES, 4, TIn>(a, total_rows);
+}
+
 template <int D, typename TIn>
 static hipError_t launch_serial_t(const PrefillArgs &a) {
   const int64_t total_rows = (int64_t)a.n_seqs * a.hv * D;
   if (total_rows == 0) return hipSuccess;
   // As for decode: four passes per wavefront when that still gives every
-  // compute unit two work-groups, else two.
+  // compute unit two work-groups, else two; eight (head sizes of 64 and up)
+  // for the largest batches, where each wavefront's input loads are then
+  // shared by more state rows.
   const int64_t blocks4 = (total_rows + (kWave / (D / 4)) * 16 - 1) / ((kWave / (D / 4)) * 16);
-  if (blocks4 < 2 * (int64_t)device_compute_units())
-    return launch_serial_p<D, 2, TIn>(a, total_rows);
-  return launch_serial_p<D, 4, TIn>(a, total_rows);
+  const int64_t cus = device_compute_units();
+  if constexpr (D >= 64) {
+    if (blocks4 >= 1024 * cus) return launch_serial_pb<D, 8, TIn>(a, total_rows);
+  }
+  if (blocks4 < 2 * cus) return launch_serial_pb<D, 2, TIn>(a, total_rows);
+  return launch_serial_pb<D, 4, TIn>(a, total_rows);
 }
 
 template <typename TIn>

@@ -98,6 +98,69 @@ def test_serial_launch_shapes(n_seqs):
     assert eo <= _o_bar("bf16") and es <= SERIAL_STATE_BAR
 
 
+@pytest.mark.parametrize("n_seqs", [3, 256])
+def test_serial_one_token(n_seqs):
+    """One token per sequence (one-token prefetch) with an initial state."""
+    dev = require_gpu()
+    x = _case((1,) * n_seqs, hqk=16, hv=32, d=128, seed=86)
+    o, sT = _run(x, dev, gdn.CHUNK_SERIAL)
+    o_ref, s_ref = _oracle(x)
+    eo, es = rel_l2(o, o_ref), rel_l2(sT, s_ref)
+    _log("serial_one_token_N%d" % n_seqs, o=eo, state=es)
+    assert eo <= _o_bar("bf16") and es <= SERIAL_STATE_BAR
+
+
+def _sampled_chains(name, x, o, sT, chains):
+    cu = x["cu_seqlens"].numpy()
+    worst_o = worst_s = 0.0
+    for n, h in chains:
+        o_ref, s_ref = oracle.prefill(**chain_slice(x, n, h))
+        worst_o = max(worst_o, rel_l2(o[cu[n]:cu[n + 1], h], o_ref[:, 0]))
+        worst_s = max(worst_s, rel_l2(sT[n, h], s_ref[0, 0]))
+    _log(name, o_max=worst_o, state_max=worst_s, chains=len(chains))
+    assert worst_o <= _o_bar("bf16") and worst_s <= SERIAL_STATE_BAR
+
+
+def test_serial_many_one_token_sequences():
+    """4096 one-token sequences at the benchmark's heads: one-token prefetch
+    and eight passes per wavefront. From a zero state one token gives
+    S = beta v k^T and o = beta v (k . q) exactly; that closed form is checked
+    for every (sequence, head), the oracle on sampled chains."""
+    dev = require_gpu()
+    n_seqs = 4096
+    x = _case((1,) * n_seqs, hqk=16, hv=32, d=128, state_std=0.0, seed=87)
+    o, sT = _run(x, dev, gdn.CHUNK_SERIAL)
+    assert torch.isfinite(o.float()).all() and torch.isfinite(sT).all()
+    grp = 2
+    k = x["k"].double().numpy()[:, np.repeat(np.arange(16), grp)]      # [N, 32, d]
+    q = x["q"].double().numpy()[:, np.repeat(np.arange(16), grp)]
+    v = x["v"].double().numpy()
+    b = x["beta"].double().numpy()
+    worst_s = worst_o = 0.0
+    for n0 in range(0, n_seqs, 256):
+        sl = slice(n0, n0 + 256)
+        s_ref = b[sl, :, None, None] * v[sl, :, :, None] * k[sl, :, None, :]
+        o_ref = b[sl, :, None] * v[sl] * np.sum(k[sl] * q[sl], axis=-1)[..., None]
+        worst_s = max(worst_s, rel_l2(sT[sl], s_ref))
+        worst_o = max(worst_o, rel_l2(o[sl], o_ref))
+    _log("serial_4096x1_closed_form", o_max=worst_o, state_max=worst_s)
+    assert worst_o <= _o_bar("bf16") and worst_s <= SERIAL_STATE_BAR
+    _sampled_chains("serial_4096x1", x, o, sT, [(n, h) for n in (0, 1777, 4095) for h in (0, 31)])
+
+
+def test_serial_many_short_sequences_with_state():
+    """2048 sequences of 1-3 tokens with initial states: four-token prefetch
+    and eight passes per wavefront, oracle on sampled chains."""
+    dev = require_gpu()
+    rng = np.random.default_rng(88)
+    lengths = tuple(int(v) for v in rng.integers(1, 4, 2048))
+    x = _case(lengths, hqk=16, hv=32, d=128, seed=88)
+    o, sT = _run(x, dev, gdn.CHUNK_SERIAL)
+    assert torch.isfinite(o.float()).all() and torch.isfinite(sT).all()
+    _sampled_chains("serial_2048x1-3", x, o, sT,
+                    [(n, h) for n in (0, 1000, 2047) for h in (0, 7, 31)])
+
+
 def test_serial_alias_in_place():
     dev = require_gpu()
     x = _case((7, 12, 1), seed=77)
