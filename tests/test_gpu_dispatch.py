@@ -210,6 +210,47 @@ def test_serial_gated(dtype):
     assert eo <= _o_bar(dtype) and es <= 1e-4
 
 
+def _gated_chain(x, n, h):
+    """Inputs of one (sequence, value head) chain of a raw-gate problem."""
+    c = chain_slice(x, n, h)
+    cu = x["cu_seqlens"].numpy()
+    t0, t1 = int(cu[n]), int(cu[n + 1])
+    return dict(q=c["q"], k=c["k"], v=c["v"], a=x["a"][t0:t1, h:h + 1],
+                b=x["b"][t0:t1, h:h + 1], a_log=x["A_log"][h:h + 1],
+                dt_bias=x["dt_bias"][h:h + 1], cu_seqlens=c["cu_seqlens"],
+                initial_state=c["initial_state"])
+
+
+@pytest.mark.parametrize("n_seqs,lengths", [(5, "ones"), (4096, "ones"), (2048, "1-3")])
+def test_serial_gated_launch_paths(n_seqs, lengths):
+    """Raw gates on the one-token prefetch path (5 and 4096 sequences of one
+    token) and on eight passes per wavefront (4096 x 1, 2048 x 1-3)."""
+    dev = require_gpu()
+    if lengths == "ones":
+        lens = (1,) * n_seqs
+    else:
+        lens = tuple(int(v) for v in np.random.default_rng(89).integers(1, 4, n_seqs))
+    x = _case(lens, hqk=16, hv=32, d=128, raw_gate=True, state_std=0.1 if n_seqs < 100 else 0.0,
+              seed=89 + n_seqs)
+    dd = to_dev(x, dev)
+    o, sT = gdn.prefill_gated(dd["q"], dd["k"], dd["v"], dd["a"], dd["b"], dd["A_log"],
+                              dd["dt_bias"], dd["cu_seqlens"],
+                              initial_state=dd["initial_state"], chunk=gdn.CHUNK_SERIAL)
+    torch.cuda.synchronize()
+    o, sT = o.cpu(), sT.cpu()
+    assert torch.isfinite(o.float()).all() and torch.isfinite(sT).all()
+    cu = x["cu_seqlens"].numpy()
+    seqs = sorted({0, n_seqs // 2, n_seqs - 1})
+    worst_o = worst_s = 0.0
+    for n in seqs:
+        for h in (0, 5, 31):
+            o_ref, s_ref = oracle.prefill_gated(**_gated_chain(x, n, h))
+            worst_o = max(worst_o, rel_l2(o[cu[n]:cu[n + 1], h], o_ref[:, 0]))
+            worst_s = max(worst_s, rel_l2(sT[n, h], s_ref[0, 0]))
+    _log("serial_gated_N%d_%s" % (n_seqs, lengths), o_max=worst_o, state_max=worst_s)
+    assert worst_o <= _o_bar("bf16") and worst_s <= 1e-4
+
+
 # ------------------------------------------------------------ chunk = 0
 @pytest.mark.parametrize("n_seqs,length", [(256, 1), (256, 3), (64, 12), (48, 40), (8, 200), (2, 400)])
 def test_auto_runs_the_reported_path(n_seqs, length):
