@@ -1,4 +1,4 @@
-"""Seeded random configurations of the prefill against the fp64 oracle.
+"""Seeded random configurations of the prefill and decode against the fp64 oracle.
 
 Each case draws a head size, a GQA grouping, a ragged batch (empty
 sequences included), a chunk setting (automatic, token-serial, 16/32/64,
@@ -63,3 +63,35 @@ def test_random_configuration(seed):
         assert eo <= (4e-3 if dtype == "bf16" else 1e-5) and es <= 2e-5
     else:
         assert eo <= O_BAR and es <= STATE_BAR
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_decode(seed):
+    """One decode step at a random batch, head size, grouping and dtype, from
+    g and beta or from the raw gate inputs (state updated in place)."""
+    dev = require_gpu()
+    rng = np.random.default_rng(3000 + seed)
+    d = int(rng.choice([32, 64, 128]))
+    hqk, hv = HEADS[int(rng.integers(len(HEADS)))]
+    B = int(rng.integers(1, 97))
+    dtype = "bf16" if rng.random() < 0.7 else "f32"
+    raw = bool(rng.random() < 0.5)
+    w = synth.DECODE_B64.replace(n_seqs=B, hqk=hqk, hv=hv, d=d, dtype=dtype, raw_gate=raw,
+                                 seed=4000 + seed)
+    x = synth.make(w)
+    dd = to_dev(x, dev)
+    state = dd["initial_state"].clone()
+    if raw:
+        o = gdn.decode_gated(dd["q"], dd["k"], dd["v"], dd["a"], dd["b"], dd["A_log"],
+                             dd["dt_bias"], state)
+        o_ref, s_ref = oracle.decode_gated(x["q"], x["k"], x["v"], x["a"], x["b"], x["A_log"],
+                                           x["dt_bias"], x["initial_state"])
+    else:
+        o = gdn.decode(dd["q"], dd["k"], dd["v"], dd["g"], dd["beta"], state)
+        o_ref, s_ref = oracle.decode(x["q"], x["k"], x["v"], x["g"], x["beta"],
+                                     x["initial_state"])
+    torch.cuda.synchronize()
+    eo, es = rel_l2(o.cpu(), o_ref), rel_l2(state.cpu(), s_ref)
+    print("[parity] random_decode%d B=%d d=%d heads=%d/%d %s raw_gates=%s o=%.3e state=%.3e"
+          % (seed, B, d, hqk, hv, dtype, raw, eo, es), flush=True)
+    assert eo <= (4e-3 if dtype == "bf16" else 1e-5) and es <= 1e-5
