@@ -86,6 +86,9 @@ def main():
                     help="skip the small-batch decode latency sweep")
     ap.add_argument("--no-dispatch-sweep", action="store_true",
                     help="skip the prefill shape-dispatch comparison over short-sequence batches")
+    ap.add_argument("--segment", type=int, default=0, metavar="L",
+                    help="force segments of L chunks in the prefill's whole-chain carry "
+                         "(0: the library's choice)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                     help="before warm-up, run a read-once/write-once kernel over MB "
                          "megabytes (three times), whose memory counters calibrate "
@@ -104,6 +107,7 @@ def main():
         sys.exit(1)
     dev = torch.device("cuda:0")
     wp, wd = synth.PREFILL_4K, synth.DECODE_B64
+    pchunk = wp.chunk | (gdn.CHUNK_SEGMENT(args.segment) if args.segment > 0 else 0)
 
     # ---------------------------------------------------------------- inputs
     P, D = [], []
@@ -114,7 +118,7 @@ def main():
         s["o"] = torch.empty((T, wp.hv, wp.d), dtype=torch.bfloat16, device=dev)
         s["fs"] = torch.empty((wp.n_seqs, wp.hv, wp.d, wp.d), device=dev)
         s["ws"] = P[0]["ws"] if P else gdn.alloc_workspace(wp.n_seqs, T, wp.hqk, wp.hv, wp.d,
-                                                             wp.chunk, dev)
+                                                             pchunk, dev)
         P.append(s)
         y = synth.make(wd, seed=wd.seed + 100 * r)
         t = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in y.items()}
@@ -133,7 +137,7 @@ def main():
 
     def run_prefill(s):
         gdn.prefill(s["q"], s["k"], s["v"], s["g"], s["beta"], s["cu_seqlens"],
-                    initial_state=s["initial_state"], chunk=wp.chunk, o=s["o"],
+                    initial_state=s["initial_state"], chunk=pchunk, o=s["o"],
                     final_state=s["fs"], workspace=s["ws"])
 
     def run_decode(t):

@@ -80,6 +80,31 @@ typedef enum gdn_dtype {
  */
 #define GDN_CHUNK_NEUMANN 0x100
 
+/*
+ * Segment length of the whole-chain carry, OR-ed into the `chunk` argument of
+ * gdn_prefill, gdn_prefill_gated and gdn_prefill_workspace_size together with
+ * a chunk size of 0, 16, 32 or 64: GDN_CHUNK_SEGMENT(L), 1 <= L <= 4095,
+ * cuts every sequence into segments of L chunks whose carries run in
+ * parallel and are joined through their affine state maps (see gdn_prefill).
+ * Without it the library picks L from the sizes. L changes only rounding and
+ * speed; the workspace size depends on it, so pass the same value to
+ * gdn_prefill_workspace_size. With chunk = 1 it is GDN_ERR_UNSUPPORTED (0 from
+ * gdn_prefill_workspace_size); with chunk = 0 it is ignored when the
+ * automatic choice is the token-serial path.
+ */
+/*
+ * The carry from chunk to chunk comes in two forms (see gdn_prefill). Without
+ * a flag the library picks one from the sizes. GDN_CHUNK_TILE_CARRY, OR-ed
+ * into `chunk` with a size of 0, 16, 32 or 64, forces the per-tile carry;
+ * GDN_CHUNK_SEGMENT(L) forces the whole-chain carry (both together is
+ * GDN_ERR_UNSUPPORTED). Same results up to rounding; the workspace size
+ * depends on the choice, so pass the same `chunk` to
+ * gdn_prefill_workspace_size.
+ */
+#define GDN_CHUNK_TILE_CARRY 0x200
+#define GDN_CHUNK_SEGMENT_SHIFT 16
+#define GDN_CHUNK_SEGMENT(L) ((int32_t)(L) << GDN_CHUNK_SEGMENT_SHIFT)
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char *gdn_status_string(gdn_status status);
 
@@ -100,7 +125,8 @@ size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
 /*
  * The chunk size gdn_prefill uses when called with chunk = 0 for these
  * sizes: 1 (token-serial), 16, 32 or 64; 0 on invalid sizes. Shape dispatch
- * after the paper's Sections 5.1 and 5.2: the choice depends on the head size,
+ * after the paper's Section 5.1 (dispatch axes) and Sections 5.3 and 5.5 (a
+ * narrow short-shape fallback): the choice depends on the head size,
  * the average sequence length T_total / N (rounded up) and N, with bounds
  * measured on MI355X. Very short sequences take the token-serial path, where
  * the chunked form's per-chunk work does not pay; longer ones take 16, 32 or
@@ -121,7 +147,7 @@ int32_t gdn_prefill_auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hqk,
  *
  * chunk = 1 runs the token-serial form instead: the recurrence token by
  * token in float32 on the vector ALU, the state held in registers for the
- * whole sequence (a short-sequence path, paper Section 5.2). chunk = 0 picks
+ * whole sequence (the narrow short-shape fallback, paper Sections 5.3 and 5.5). chunk = 0 picks
  * one of the sizes as gdn_prefill_auto_chunk() reports.
  *
  *   q, k, v, g, beta, cu_seqlens : inputs, layouts above.

@@ -40,7 +40,7 @@ gdn_status check_heads(int32_t hqk, int32_t hv) {
 
 // Shape dispatch of the prefill (the paper's Section 5.1: the chunk size is
 // chosen from the number of sequences, the total tokens and the average
-// sequence length; Section 5.2: a narrow token-serial path for tiny shapes).
+// sequence length; Sections 5.3 and 5.5: a narrow short-shape fallback).
 // The rule is a table per head size on the average length T/N (rounded up)
 // and the number of sequences N: the token-serial path up to `serial`
 // tokens, or up to `serial_big` when N >= n_big; then chunks of 16, 32 and
@@ -69,12 +69,44 @@ int32_t auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t d) {
   return 64;
 }
 
+// The `chunk` argument: a size (0, 1, 16, 32, 64), optionally OR-ed with
+// GDN_CHUNK_NEUMANN and GDN_CHUNK_SEGMENT(L). `ok` is false when other bits
+// are set.
+struct ChunkArg {
+  int32_t size;
+  bool neumann;
+  bool tiles;   // GDN_CHUNK_TILE_CARRY: the per-tile carry
+  int32_t seg;  // requested chunks per segment (whole-chain carry), 0 = automatic
+  bool ok;
+};
+ChunkArg parse_chunk(int32_t chunk) {
+  ChunkArg c;
+  const uint32_t u = (uint32_t)chunk;
+  const uint32_t seg_mask = 0xfffu << GDN_CHUNK_SEGMENT_SHIFT;
+  c.size = (int32_t)(u & 0xffu);
+  c.neumann = (u & GDN_CHUNK_NEUMANN) != 0;
+  c.tiles = (u & GDN_CHUNK_TILE_CARRY) != 0;
+  c.seg = (int32_t)((u & seg_mask) >> GDN_CHUNK_SEGMENT_SHIFT);
+  c.ok = (u & ~(0xffu | (uint32_t)GDN_CHUNK_NEUMANN | (uint32_t)GDN_CHUNK_TILE_CARRY | seg_mask)) == 0 &&
+         !(c.tiles && c.seg > 0);
+  return c;
+}
+
+// The carry of a chunked call: the per-tile carry when forced, or when no
+// segment length is forced and the batch has few chains.
+bool tile_carry(const ChunkArg &c, int32_t n_seqs, int32_t hv, int32_t d) {
+  return c.tiles || (c.seg == 0 && gdn::uses_tile_carry(n_seqs, hv, d));
+}
+
 // Workspace bytes for a resolved chunk size. The token-serial path uses none;
 // it reports the 256-byte minimum so that 0 keeps meaning "invalid sizes".
 size_t required_workspace(int32_t n_seqs, int64_t n_tokens, int32_t hqk, int32_t hv, int32_t d,
-                       int32_t chunk) {
+                          int32_t chunk, const ChunkArg &c) {
   if (chunk == 1) return 256;
-  return gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, d, chunk).total;
+  const int L = gdn::chain_segment_chunks(n_tokens, hv, chunk, c.seg);
+  return gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, d, chunk, L,
+                                       tile_carry(c, n_seqs, hv, d))
+      .total;
 }
 
 // The gate inputs: either g and beta, or all four raw inputs of the gated
@@ -95,18 +127,24 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
   if (check_heads(hqk, hv) != GDN_OK) return GDN_ERR_INVALID_ARG;
   if (dk <= 0 || dv <= 0) return GDN_ERR_INVALID_ARG;
   // GDN_CHUNK_NEUMANN selects the Neumann-product diagonal inverse of the
-  // chunked path; it is meaningless for the token-serial path.
-  const bool neumann = (chunk & GDN_CHUNK_NEUMANN) != 0;
-  chunk &= ~GDN_CHUNK_NEUMANN;
+  // chunked path; it is meaningless for the token-serial path. A segment
+  // length applies to the chunked path and is ignored when the automatic
+  // choice is the token-serial path.
+  const ChunkArg ca = parse_chunk(chunk);
+  if (!ca.ok) return GDN_ERR_UNSUPPORTED;
+  const bool neumann = ca.neumann;
+  chunk = ca.size;
   if (chunk == 0 && !neumann) chunk = auto_chunk(n_seqs, n_tokens, dk);
   if (!supported_head(dk, dv) || !supported_chunk(chunk) || !supported_dtype(dtype) ||
-      (neumann && chunk < 16))
+      (neumann && chunk < 16) || ((ca.seg > 0 || ca.tiles) && ca.size == 1))
     return GDN_ERR_UNSUPPORTED;
   if (n_seqs == 0) return n_tokens == 0 ? GDN_OK : GDN_ERR_INVALID_ARG;
   if (!cu_seqlens || !final_state) return GDN_ERR_INVALID_ARG;
   if (n_tokens > 0 && (!q || !k || !v || !o || !gate_present(g, beta, gate)))
     return GDN_ERR_INVALID_ARG;
-  if (!workspace || workspace_bytes < required_workspace(n_seqs, n_tokens, hqk, hv, dk, chunk) ||
+  const int seg_chunks = chunk == 1 ? 0 : gdn::chain_segment_chunks(n_tokens, hv, chunk, ca.seg);
+  if (!workspace ||
+      workspace_bytes < required_workspace(n_seqs, n_tokens, hqk, hv, dk, chunk, ca) ||
       (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
     return GDN_ERR_WORKSPACE;
 
@@ -123,14 +161,17 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
   a.neumann = neumann;
   // The single-wave carry when the average sequence fits in one chunk: a
   // work-group carry's fixed cost then outweighs its per-chunk speed.
-  a.wave_carry = n_tokens <= (int64_t)n_seqs * chunk;
+  a.wave_carry = gdn::uses_wave_carry(n_seqs, n_tokens, chunk);
+  a.seg_chunks = seg_chunks;
+  a.tile_carry = tile_carry(ca, n_seqs, hv, dk);
   a.dtype = dtype;
   a.workspace = workspace;
   a.stream = stream;
   const hipError_t e =
       chunk == 1 ? gdn::launch_prefill_serial(a)
-                 : gdn::launch_prefill(
-                       a, gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, dk, chunk));
+                 : gdn::launch_prefill(a, gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk,
+                                                                        hv, dk, chunk, seg_chunks,
+                                                                        a.tile_carry));
   return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
 }
 
@@ -173,7 +214,7 @@ const char *gdn_status_string(gdn_status status) {
   return "unknown status";
 }
 
-int gdn_version(void) { return 1 * 10000 + 2 * 100 + 0; }
+int gdn_version(void) { return 1 * 10000 + 3 * 100 + 0; }
 
 size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
                                   int32_t hqk, int32_t hv, int32_t dk,
@@ -181,20 +222,19 @@ size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
   if (n_seqs < 0 || n_tokens < 0 || n_tokens > INT32_MAX) return 0;
   if (check_heads(hqk, hv) != GDN_OK) return 0;
   if (!supported_head(dk, dv)) return 0;
-  if (chunk & GDN_CHUNK_NEUMANN) {  // same tables as the plain chunked path
-    chunk &= ~GDN_CHUNK_NEUMANN;
-    if (chunk < 16) return 0;
-  }
-  if (chunk == 0) {  // enough for whichever size the dispatch picks
+  const ChunkArg ca = parse_chunk(chunk);
+  if (!ca.ok || (ca.neumann && ca.size < 16) || ((ca.seg > 0 || ca.tiles) && ca.size == 1))
+    return 0;
+  if (ca.size == 0 && !ca.neumann) {  // enough for whichever size the dispatch picks
     size_t m = 0;
     for (int32_t c : {1, 16, 32, 64}) {
-      const size_t b = required_workspace(n_seqs, n_tokens, hqk, hv, dk, c);
+      const size_t b = required_workspace(n_seqs, n_tokens, hqk, hv, dk, c, ca);
       m = b > m ? b : m;
     }
     return m;
   }
-  if (!supported_chunk(chunk)) return 0;
-  return required_workspace(n_seqs, n_tokens, hqk, hv, dk, chunk);
+  if (!supported_chunk(ca.size)) return 0;
+  return required_workspace(n_seqs, n_tokens, hqk, hv, dk, ca.size, ca);
 }
 
 int32_t gdn_prefill_auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hqk, int32_t hv,

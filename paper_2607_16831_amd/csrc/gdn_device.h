@@ -23,8 +23,12 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
   __bf16 b = (__bf16)x;  // v_cvt_pk_bf16_f32: round to nearest even
   return __builtin_bit_cast(uint16_t, b);
 }
+// Two floats rounded to nearest even into one packed bf16 pair (lo in the
+// low half): a single v_cvt_pk_bf16_f32.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)f32_to_bf16_bits(lo) | ((uint32_t)f32_to_bf16_bits(hi) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
 }
 
 // Eight consecutive elements of a row, returned as packed bf16 (16 bytes).

@@ -39,6 +39,8 @@ struct PrefillArgs {
   int hqk, hv, d, chunk;
   bool neumann;  // diagonal blocks of the WY factor by the Neumann product
   bool wave_carry;  // single-wave carry (batches of short sequences)
+  int seg_chunks;   // chunks per segment of the whole-chain carry
+  bool tile_carry;  // bf16: the per-tile carry instead of the whole-chain carry
   gdn_dtype dtype;
   void *workspace;
   hipStream_t stream;
@@ -49,8 +51,13 @@ struct PrefillWorkspace {
   size_t decay;       // f32  [chunks, HV, 2, C]: exp(gamma_i), exp(gamma_last - gamma_i)
   size_t tfrag;       // bf16 [chunks, HV, FRAG]: (I + A)^-1 in operand order
   size_t pfrag;       // bf16 [chunks, HV, FRAG]: decay-masked Q K^T, same order
-  size_t qfrag;       // bf16 [chunks, HQK, C * D]: Q in operand order
+  size_t qfrag;       // bf16 [chunks, HQK, C * D]: Q in operand order (per-tile carry)
   size_t kcopy;       // bf16 [chunks, HQK, C, D]: K rounded to bf16 (f32 inputs)
+  // Segment maps of the whole-chain carry (n_maps slots; none when no
+  // sequence can span more than one segment):
+  size_t bslot;       // f32  [n_maps, HV, D, D]: B of a segment, then the composed state
+  size_t mthi, mtlo;  // bf16 [n_maps, HV, D, D]: M^T of a segment, hi and lo parts
+  int64_t n_maps;
   size_t total;
 };
 
@@ -63,13 +70,33 @@ inline int64_t frag_elems(int chunk) {
 inline int64_t chunk_bound(int n_seqs, int64_t n_tokens, int chunk) {
   return (n_tokens + chunk - 1) / chunk + n_seqs;
 }
+// Chunks per segment of the whole-chain carry: `requested` if positive, else
+// enough that the segments of all chains give about kChainUnits work-groups.
+constexpr int kChainUnits = 256;
+// Largest number of 16-row value tiles (sequences x value heads x D/16) for
+// which the per-tile carry is chosen.
+constexpr int64_t kTileCarryMaxTiles = 256;
+constexpr int kMinSegmentChunks = 4;
+int chain_segment_chunks(int64_t n_tokens, int hv, int chunk, int requested);
+// The whole-chain carry runs unless the average sequence fits in one chunk
+// (then the single-wave carry does).
+inline bool uses_wave_carry(int n_seqs, int64_t n_tokens, int chunk) {
+  return n_tokens <= (int64_t)n_seqs * chunk;
+}
+// The per-tile carry when the batch has few (sequence, value head) chains:
+// every chain is then spread over D/16 work-groups without segments.
+bool uses_tile_carry(int n_seqs, int hv, int d);
 PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
-                                          int hv, int d, int chunk);
+                                          int hv, int d, int chunk, int seg_chunks, bool tile);
 
 hipError_t launch_decode(const DecodeArgs &a);
 // Chunked prefill (chunk 16, 32 or 64) and the token-serial prefill (chunk 1,
 // no workspace).
 hipError_t launch_prefill(const PrefillArgs &a, const PrefillWorkspace &ws);
+// The whole-chain carry and the per-tile carry (bf16 inputs), after the
+// chunk-local kernel.
+hipError_t launch_chain_d(const PrefillArgs &a, const PrefillWorkspace &ws);
+hipError_t launch_tile_carry(const PrefillArgs &a, const PrefillWorkspace &ws);
 hipError_t launch_prefill_serial(const PrefillArgs &a);
 
 // Compute units of the current device, read once per process.

@@ -28,62 +28,13 @@
 //
 // Every exponent is a non-positive difference (for g <= 0), masked before
 // exp, so strongly decaying inputs cannot overflow.
-#include "gdn_device.h"
+#include <algorithm>
+
 #include "gdn_launch.h"
+#include "prefill_common.h"
 
 namespace gdn {
 
-// ============================================================ chunk numbering
-// Chunks get global slots without a scan: sequence n owns the slots
-// cu[n] / C + n + [0, ceil(len_n / C)). Consecutive ranges never overlap
-// (cu[n+1] / C + n + 1 >= cu[n] / C + n + ceil(len_n / C)) and every slot is
-// below ceil(T / C) + N, so per-chunk tables sized by that bound suffice.
-__device__ __forceinline__ int64_t first_slot(const int32_t *cu, int n, int chunk) {
-  return (int64_t)cu[n] / chunk + n;
-}
-
-template <int D, int C>
-struct Cfg {
-  static constexpr int NIB = C / 16;           // 16-token blocks per chunk
-  static constexpr int KS = (C + 31) / 32;     // 32-token contraction steps
-  static constexpr int CP = KS * 32;           // chunk padded to the step
-  static constexpr int DS = D / 32;            // 32-wide steps over the head dim
-  static constexpr int NKT = D / 16;           // 16-wide key tiles of the state
-  static constexpr int KTW = (NKT + 3) / 4;    // key tiles per wavefront
-  static constexpr int NVT = D / 16;           // 16-row value tiles per head
-  static constexpr int LDK = D + 8;            // bf16 pitch, padded K/Q tiles
-  static constexpr int LDA = C + 4;            // f32 pitch, C x C tiles
-  static constexpr int LDV = CP + 8;           // bf16 pitch, [value][token] tiles
-  static constexpr int FRAG = NIB * KS * 512;  // bf16 elements per C x C operand
-  static constexpr int PIECES = (C / 4) * (D / 8);  // 4-row x 8-column K pieces
-  static_assert(PIECES <= 256, "one K piece per thread");
-  static_assert(C % 16 == 0 && C <= 64 && D % 32 == 0 && D <= 128, "shape");
-};
-
-// Every contraction over the tokens of a chunk (T Y, P U, K^T Uh) uses one
-// order of the tokens inside each 32-token block: position p = 8 g + 4 h + e
-// holds token j = 16 h + 4 g + e (g, e in [0, 4), h in {0, 1}). It is the
-// order in which a 16x16 accumulator tile pair hands out its rows, so tiles
-// produced by one product feed the next without a transpose.
-__device__ __forceinline__ int tok_pos(int j) {
-  const int r = j & 31;
-  return (j & ~31) + 8 * ((r >> 2) & 3) + 4 * (r >> 4) + (r & 3);
-}
-
-// ============================================================ swizzled tiles
-// Element index of (row, column) in a swizzled row-major [rows][D] bf16 tile:
-// 16-byte chunks are XORed with a row function so that 16 consecutive rows
-// at one column (matrix-operand reads) fall on distinct bank groups.
-template <int D>
-__device__ __forceinline__ int kn_swizzle(int row) {
-  return ((row & 15) ^ ((row >> 4) & 3)) & (D / 8 - 1);
-}
-template <int D>
-__device__ __forceinline__ int kn_index(int row, int col) {
-  return row * D + 8 * ((col >> 3) ^ kn_swizzle<D>(row)) + (col & 7);
-}
-
-typedef __attribute__((address_space(3))) void lds_void;
 
 // ============================================================ chunk-local
 // One work-group per (chunk, value head): gamma, K K^T and K Q^T, then A, P
@@ -296,17 +247,19 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  // ---- Q of this chunk for the carry, in the A-operand order of Q S^T:
-  // block ib, step s, lane (l16, g4) holds Q[16 ib + l16][32 s + 8 g4 + (0..7)].
-  // For f32 inputs also a bf16 copy of K, row-major [C][D], for the carry.
-  // One value head of the group writes them.
+  // ---- for the per-tile carry (qfrag not null): Q of this chunk in the
+  // A-operand order of Q S^T, block ib, step s, lane (l16, g4) holding
+  // Q[16 ib + l16][32 s + 8 g4 + (0..7)]. For f32 inputs: a bf16 copy of K,
+  // row-major [C][D], for the carry. One value head of the group writes them.
   if (gi == 0 && wave < NIB) {
     const int64_t base = ((int64_t)cidx * hqk + hk) * (C * D);
-    uint16_t *qf = qfrag + base + ((int64_t)wave * F::DS * 64 + lane) * 8;
+    if (qfrag != nullptr) {
+      uint16_t *qf = qfrag + base + ((int64_t)wave * F::DS * 64 + lane) * 8;
 #pragma unroll
-    for (int s = 0; s < F::DS; ++s)
-      *reinterpret_cast<uint4 *>(qf + s * 512) =
-          *reinterpret_cast<const uint4 *>(&Qt[kn_index<D>(16 * wave + l16, 32 * s + 8 * g4)]);
+      for (int s = 0; s < F::DS; ++s)
+        *reinterpret_cast<uint4 *>(qf + s * 512) =
+            *reinterpret_cast<const uint4 *>(&Qt[kn_index<D>(16 * wave + l16, 32 * s + 8 * g4)]);
+    }
     if (sizeof(TIn) == 4) {
       uint16_t *kc = kcopy + base + (int64_t)(16 * wave + l16) * D;
 #pragma unroll
@@ -475,547 +428,6 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   }
 }
 
-// ============================================================ chunk carry
-// One work-group per (sequence, value head, 16-row value tile): ten
-// wavefronts, eight that compute and two that only move data.
-//
-// Compute wavefronts 0-3 own token block w of the chunk for X = K S^T, Y and
-// U = T' Y; wavefronts 4-7 own token block w - 4 for Q S^T and O; all eight
-// update one 16-key tile of the state each. The operands only one wavefront
-// needs (its rows of T', P and Q, stored by the chunk-local kernel in operand
-// order) are loaded straight into its registers one chunk ahead, 1 KB per
-// contiguous load. What several wavefronts share goes through LDS: K (rows
-// for X, columns for the state update), the V tile and the decay factors,
-// copied by the two loader wavefronts with buffer-to-LDS loads into a buffer
-// the compute wavefronts are not reading.
-//
-// Per chunk, three phases separated by work-group barriers carry the chain
-// X -> Y -> U -> state; each phase reads from LDS only what the phase before
-// produced (S^T, Y, U). Everything else a phase needs -- K rows and K^T
-// operands, V and the decay factors -- is read into registers a phase or
-// more ahead: waves 0-3 read those of chunk c + 1 right after the state
-// update of chunk c (the reads stay in flight across the barrier), waves
-// 4-7 their K^T operands in phase 1. Outputs go from registers straight to
-// global memory.
-//
-// Global reads go through buffer resources: rows past the end of the
-// sequence read as zero (beta is zero there, so they add exact zeros) and
-// stores past the end are dropped by the resource extent.
-template <int D, int C, typename TIn>
-struct CarryCfg {
-  using F = Cfg<D, C>;
-  static constexpr int NCW = 8;                  // compute wavefronts
-  static constexpr int NLW = 2;                  // loader wavefronts
-  static constexpr int NT = 64 * (NCW + NLW);    // threads
-  static constexpr int ESZ = (int)sizeof(TIn);
-  static constexpr int KPR = D / 8;              // 16-byte units per bf16 K row
-  static constexpr int NKI = C * D / 512;        // 1 KB copies per K chunk
-  static constexpr int VPR = ESZ;                // 16-byte units per token of a V tile row
-  static constexpr int VU = C * VPR;             // 16-byte units of the V tile
-  static constexpr int NVI = (VU + 63) / 64;     // 1 KB copies per V tile
-  static constexpr int NDI = (2 * C + 255) / 256;  // 1 KB copies of the 2C decay factors
-  static constexpr int M = NKI + NVI + NDI;      // copies per chunk
-  static constexpr int SLOTS = (M + NLW - 1) / NLW;
-  static constexpr int NB = 4;                   // LDS buffers of the copied inputs
-  static constexpr int NA = NB - 1;              // chunks issued ahead of the one in use
-  static_assert(NT == 640, "launch bounds of the carry kernel");
-};
-
-constexpr int kCarryThreads = 640;
-
-template <int D, int C, typename TIn>
-struct CarryLds {
-  using F = Cfg<D, C>;
-  using CC = CarryCfg<D, C, TIn>;
-  // The copied inputs of chunk lc live in buffer lc % NB.
-  uint16_t Kn[CC::NB][F::CP * D];  // K chunk, row-major, swizzled; rows C..CP-1 stay zero
-  uint4 Vl[CC::NB][CC::NVI * 64];  // V tile, [token][16 values], input element type
-  float Dl[CC::NB][CC::NDI * 256];  // exp(gamma_i), then exp(gamma_last - gamma_i)
-  uint16_t Sl[16 * F::LDK];     // bf16 copy of the state tile, [value][key]
-  uint16_t Yl[16 * F::LDV];     // Y,  [value][token position]
-  uint16_t Ul[16 * F::LDV];     // U,  [value][token position]
-  uint16_t Uh[16 * F::LDV];     // exp(gamma_last - gamma) U, same layout
-};
-
-__device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) {
-  return make_uint2(pack_bf16x2(a, b), pack_bf16x2(c, d));
-}
-
-typedef short v4i16 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-
-// K^T as the A operand of the state update for key tile t, token step s:
-// lane (l16, g4) gets K[j][16 t + l16] for the 8 tokens at positions
-// 32 s + 8 g4 + [0, 8). Each transpose load serves 4 tokens: lanes 4m..4m+3
-// of a 16-lane group point at token j_m, key columns 16 t + 4 (l16 % 4) + [0,4).
-template <int D>
-__device__ __forceinline__ uint4 kt_operand(const uint16_t *Kn, int t, int s,
-                                            int l16, int g4) {
-  uint32_t w[4];
-#pragma unroll
-  for (int hh = 0; hh < 2; ++hh) {
-    const int j = 32 * s + 16 * hh + 4 * g4 + (l16 >> 2);
-    const uint16_t *p = Kn + kn_index<D>(j, 16 * t + 4 * (l16 & 3));
-    const v4i16 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_v4i16 *)(const_cast<uint16_t *>(p)));
-    w[2 * hh] = (uint32_t)(uint16_t)x[0] | ((uint32_t)(uint16_t)x[1] << 16);
-    w[2 * hh + 1] = (uint32_t)(uint16_t)x[2] | ((uint32_t)(uint16_t)x[3] << 16);
-  }
-  return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
-constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond every resource: reads 0
-
-// ---------------------------------------------------------------- loaders
-// Copy m of a chunk, in order: K, V tile, decay factors, each 16 bytes per
-// lane (1 KB per copy). A buffer-to-LDS load writes lane i's bytes at
-// LDS base + i * size, so the per-lane source offset chooses what lands
-// where: for K it undoes the row swizzle. The offsets do not change from
-// chunk to chunk.
-template <int D, int C, typename TIn>
-__device__ __forceinline__ uint32_t copy_offset(int m, int lane, int kstride, int hv) {
-  using CC = CarryCfg<D, C, TIn>;
-  if (m < CC::NKI) {
-    const int u = 64 * m + lane, row = u / CC::KPR;
-    const int jl = (u % CC::KPR) ^ kn_swizzle<D>(row);
-    return (uint32_t)((row * kstride + 8 * jl) * 2);
-  } else if (m < CC::NKI + CC::NVI) {
-    const int u = 64 * (m - CC::NKI) + lane;
-    if (u >= CC::VU) return kOutOfRange;
-    return (uint32_t)(((u / CC::VPR) * hv * D + (u % CC::VPR) * (16 / CC::ESZ)) * CC::ESZ);
-  } else if (m < CC::M) {
-    const int u = 64 * (m - CC::NKI - CC::NVI) + lane;  // 4 factors per lane
-    return 4 * u < 2 * C ? (uint32_t)(16 * u) : kOutOfRange;
-  }
-  return kOutOfRange;
-}
-
-struct CopyRes {
-  rsrc_t k, v, d;
-};
-
-template <int D, int C, typename TIn>
-__device__ __forceinline__ void issue_copy(CarryLds<D, C, TIn> &L, int bb, const CopyRes &R,
-                                           int m, uint32_t off) {
-  using CC = CarryCfg<D, C, TIn>;
-  if (m < CC::NKI) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(R.k, (lds_void *)&L.Kn[bb][512 * m], 16, off, 0, 0, 0);
-  } else if (m < CC::NKI + CC::NVI) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(R.v, (lds_void *)&L.Vl[bb][64 * (m - CC::NKI)], 16, off, 0, 0, 0);
-  } else if (m < CC::M) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(R.d, (lds_void *)&L.Dl[bb][256 * (m - CC::NKI - CC::NVI)], 16, off, 0, 0, 0);
-  }
-}
-
-// Copies loader LW issues per chunk.
-template <int D, int C, typename TIn, int LW>
-constexpr int loader_copies() {
-  using CC = CarryCfg<D, C, TIn>;
-  int n = 0;
-  for (int i = 0; i < CC::SLOTS; ++i) n += (CC::NLW * i + LW < CC::M) ? 1 : 0;
-  return n;
-}
-
-// Waits until at most N of this wavefront's vector-memory operations are
-// outstanding (they complete in issue order).
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// Work-group barrier that lets the youngest N LDS operations of this
-// wavefront stay in flight. LDS operations complete in issue order, so every
-// LDS access issued before those N (a state write, say) is complete and
-// visible to the other wavefronts after the barrier.
-template <int N>
-__device__ __forceinline__ void lds_barrier_keep() {
-  static_assert(N >= 0 && N <= 15, "LDS counter range");
-  asm volatile("s_waitcnt lgkmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
-}
-
-// Loader wavefront LW (a template parameter, so that the kind of each of its
-// copies is known when compiling). The copies of chunk lc + NA are issued at
-// the start of chunk lc into the buffer chunk lc - 1 used, and chunk lc + 1
-// must have landed before the second barrier of chunk lc: waves 0-3 read it
-// in phase 3.
-template <int D, int C, typename TIn, int LW>
-__device__ __forceinline__ void carry_loader(
-    CarryLds<D, C, TIn> &L, int lane, const uint16_t *__restrict__ ksrc, int kstride,
-    bool kcopied, const TIn *__restrict__ v, const float *__restrict__ dec_ws, int nch,
-    int64_t seq_t0, int64_t seq_t1, int64_t c0, int h, int hk, int hqk, int hv, int v0) {
-  using CC = CarryCfg<D, C, TIn>;
-  constexpr int NS = CC::SLOTS;
-  uint32_t off[NS];
-#pragma unroll
-  for (int i = 0; i < NS; ++i) off[i] = copy_offset<D, C, TIn>(CC::NLW * i + LW, lane, kstride, hv);
-
-  auto res = [&](int lc) {
-    const int64_t t0 = seq_t0 + (int64_t)lc * C;
-    const int nv = (int)min((int64_t)C, seq_t1 - t0);
-    CopyRes r;
-    if (kcopied)  // bf16 copy in the workspace, [chunk slot][key head][C][D]
-      r.k = make_rsrc(ksrc + ((c0 + lc) * hqk + hk) * (C * D), C * D * 2);
-    else
-      r.k = make_rsrc(ksrc + (t0 * hqk + hk) * D, (uint32_t)(nv * hqk * D * 2));
-    r.v = make_rsrc(v + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * CC::ESZ));
-    r.d = make_rsrc(dec_ws + ((c0 + lc) * hv + h) * 2 * C, 2 * C * 4);
-    return r;
-  };
-
-  constexpr int NCP = loader_copies<D, C, TIn, LW>();
-  constexpr int NA = CC::NA;
-  auto issue = [&](int lc) {  // chunk lc into buffer lc % NB
-    const CopyRes R = res(lc);
-#pragma unroll
-    for (int i = 0; i < NS; ++i) issue_copy<D, C, TIn>(L, lc % CC::NB, R, CC::NLW * i + LW, off[i]);
-  };
-#pragma unroll
-  for (int j = 0; j < NA; ++j)
-    if (j < nch) issue(j);
-  if (nch >= NA)
-    wait_vm<(NA - 1) * NCP>();  // chunk 0 has landed
-  else
-    wait_vm<0>();
-  lds_barrier();
-
-  for (int lc = 0; lc < nch; ++lc) {
-    if (lc + NA < nch) issue(lc + NA);
-    lds_barrier();
-    // Chunk lc + 1 must have landed. While copies are still issued every
-    // chunk, those of the NA - 1 later chunks may stay in flight; near the
-    // end everything is waited for.
-    if (lc + NA < nch)
-      wait_vm<(NA - 1) * NCP>();
-    else
-      wait_vm<0>();
-    lds_barrier();
-    lds_barrier();
-  }
-}
-
-// ---------------------------------------------------------------- compute
-// Per chunk c, three phases separated by work-group barriers:
-//   1. waves 0-3: X = K S^T for their token block, Y = V - exp(gamma) X.
-//      waves 4-7: O of chunk c-1 = exp(gamma) Q S^T + P U (their operands
-//      were kept from chunk c-1; U of chunk c-1 is still in LDS), stored to
-//      global memory; the K^T operands of chunk c.
-//   2. waves 0-3: U = T' Y and exp(gamma_last - gamma) U.
-//      waves 4-7: Q S^T (S is still the state entering chunk c).
-//   3. all eight: S^T <- exp(gamma_last) S^T + K^T (exp(gamma_last - gamma) U)
-//      for their key tile; waves 0-3 then read chunk c + 1's operands.
-// The chain from one state to the next runs through phases 1-3 on waves 0-3
-// and the update; the output work fills the phases where it would idle.
-template <int D, int C, typename TIn>
-__device__ __forceinline__ void state_update(CarryLds<D, C, TIn> &L, f32x4 &S, const uint4 *kt,
-                                             float glast, int wave, int l16, int g4) {
-  using F = Cfg<D, C>;
-  uint4 bu[F::KS];
-#pragma unroll
-  for (int s = 0; s < F::KS; ++s)
-    bu[s] = *reinterpret_cast<const uint4 *>(&L.Uh[l16 * F::LDV + 32 * s + 8 * g4]);
-  f32x4 acc = S * glast;
-  __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-  for (int s = 0; s < F::KS; ++s) acc = mfma_16x16x32(kt[s], bu[s], acc);
-  S = acc;
-  *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
-      pack4_bf16(acc[0], acc[1], acc[2], acc[3]);
-}
-
-// Wavefronts 0-3: X, Y and U for token block ib. Each role runs its own loop
-// (with the same barriers) so that every register prefetched for the next
-// chunk is consumed and then reloaded in place.
-template <int D, int C, typename TIn>
-__device__ __forceinline__ void carry_compute_xu(
-    CarryLds<D, C, TIn> &L, f32x4 &S, int wave, int lane, int nch, int64_t c0,
-    const uint16_t *__restrict__ tfrag, int h, int hv) {
-  using F = Cfg<D, C>;
-  using CC = CarryCfg<D, C, TIn>;
-  const int l16 = lane & 15, g4 = lane >> 4;
-  const int ib = wave;
-  const bool blk = (F::NIB == 4) || (ib < F::NIB);
-  const bool own = (F::NKT == 8) || (wave < F::NKT);
-  const int ibc = min(ib, F::NIB - 1);
-  // T' fragments of block ibc on or below the diagonal; the others are zero,
-  // never stored, and read through an offset past the resource (zeros).
-  const int nks = min(ibc / 2 + 1, F::KS);
-  const int tb = 16 * ibc + 4 * g4;                     // this lane's first token
-  const int ypos = 32 * (ib >> 1) + 8 * g4 + 4 * (ib & 1);  // tok_pos(16 ib + 4 g4)
-  const uint32_t foff = (uint32_t)(((ibc * F::KS) * 64 + lane) * 16);
-  auto frag_res = [&](int lc) {
-    return make_rsrc(tfrag + ((c0 + lc) * hv + h) * F::FRAG, F::FRAG * 2);
-  };
-  // operands of the chunk in use, read ahead
-  uint4 fa[F::KS];   // T' rows of block ib (global)
-  uint4 ka[F::DS];   // K rows of block ib (LDS)
-  uint4 kt[F::KS];   // K^T operands of key tile `wave` (LDS)
-  float vv[4], ge[4], he[4], glast = 0.f;
-  auto fetch_lds = [&](int b) {  // V, decay factors, then K^T and K rows of buffer b
-    if (blk) {
-      const TIn *vt = reinterpret_cast<const TIn *>(L.Vl[b]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) vv[e] = Elem<TIn>::load1(&vt[(tb + e) * 16 + l16]);
-      const float4 ge4 = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
-      const float4 he4 = *reinterpret_cast<const float4 *>(&L.Dl[b][C + tb]);
-      ge[0] = ge4.x; ge[1] = ge4.y; ge[2] = ge4.z; ge[3] = ge4.w;
-      he[0] = he4.x; he[1] = he4.y; he[2] = he4.z; he[3] = he4.w;
-    }
-    glast = L.Dl[b][C - 1];
-    if (own) {
-#pragma unroll
-      for (int s = 0; s < F::KS; ++s) kt[s] = kt_operand<D>(L.Kn[b], wave, s, l16, g4);
-    }
-    if (blk) {
-#pragma unroll
-      for (int s = 0; s < F::DS; ++s)
-        ka[s] = *reinterpret_cast<const uint4 *>(&L.Kn[b][kn_index<D>(16 * ib + l16, 32 * s + 8 * g4)]);
-    }
-  };
-  {
-    const rsrc_t rt = frag_res(0);
-#pragma unroll
-    for (int s = 0; s < F::KS; ++s) fa[s] = buf_load_b128(rt, s < nks ? foff + 1024u * s : kOutOfRange);
-  }
-  fetch_lds(0);
-  for (int lc = 0; lc < nch; ++lc) {
-    // ---- phase 1: X = K S^T, Y = V - exp(gamma) X (beta is folded into T')
-    if (blk) {
-      uint4 bs[F::DS];
-#pragma unroll
-      for (int s = 0; s < F::DS; ++s)
-        bs[s] = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
-      __builtin_amdgcn_sched_barrier(0);
-      f32x4 xs = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < F::DS; ++s) xs = mfma_16x16x32(ka[s], bs[s], xs);
-      *reinterpret_cast<uint2 *>(&L.Yl[l16 * F::LDV + ypos]) =
-          pack4_bf16(vv[0] - ge[0] * xs[0], vv[1] - ge[1] * xs[1], vv[2] - ge[2] * xs[2],
-                     vv[3] - ge[3] * xs[3]);
-    }
-    lds_barrier();
-    // ---- phase 2: U = T' Y and exp(gamma_last - gamma) U
-    if (blk) {
-      uint4 by[F::KS];
-#pragma unroll
-      for (int s = 0; s < F::KS; ++s)
-        by[s] = *reinterpret_cast<const uint4 *>(&L.Yl[l16 * F::LDV + 32 * s + 8 * g4]);
-      __builtin_amdgcn_sched_barrier(0);
-      f32x4 u = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < F::KS; ++s) u = mfma_16x16x32(fa[s], by[s], u);
-      *reinterpret_cast<uint2 *>(&L.Ul[l16 * F::LDV + ypos]) = pack4_bf16(u[0], u[1], u[2], u[3]);
-      *reinterpret_cast<uint2 *>(&L.Uh[l16 * F::LDV + ypos]) =
-          pack4_bf16(he[0] * u[0], he[1] * u[1], he[2] * u[2], he[3] * u[3]);
-      // reload after the last reader (the last chunk re-reads itself)
-      __builtin_amdgcn_sched_barrier(0);
-      const rsrc_t rt = frag_res(min(lc + 1, nch - 1));
-#pragma unroll
-      for (int s = 0; s < F::KS; ++s) fa[s] = buf_load_b128(rt, s < nks ? foff + 1024u * s : kOutOfRange);
-    }
-    lds_barrier();
-    // ---- phase 3: state update, then chunk lc + 1's LDS operands, whose
-    // K^T and K reads may stay in flight across the barrier
-    if (own) {
-      state_update<D, C, TIn>(L, S, kt, glast, wave, l16, g4);
-      asm volatile("" ::"v"(S) : "memory");
-    }
-    if (lc + 1 < nch) {
-      fetch_lds((lc + 1) % CC::NB);
-      lds_barrier_keep<((F::NKT == 8) ? 2 * F::KS : 0) + ((F::NIB == 4) ? F::DS : 0)>();
-    } else {
-      lds_barrier();
-    }
-  }
-}
-
-// Wavefronts 4-7: the K^T operands of the chunk and the output of the
-// previous one in phase 1, Q S^T in phase 2, O = exp(gamma) Q S^T + P U
-// for token block ib (U of that chunk is still in LDS in the next phase 1).
-template <int D, int C, typename TIn>
-__device__ __forceinline__ void carry_compute_o(
-    CarryLds<D, C, TIn> &L, f32x4 &S, int wave, int lane, int nch, int64_t c0,
-    const uint16_t *__restrict__ pfrag, const uint16_t *__restrict__ qfrag,
-    TIn *__restrict__ o, int64_t seq_t0, int64_t seq_t1, int h, int hk, int hqk, int hv,
-    int v0) {
-  using F = Cfg<D, C>;
-  using CC = CarryCfg<D, C, TIn>;
-  const int l16 = lane & 15, g4 = lane >> 4;
-  const int ib = wave - 4;
-  const bool blk = (F::NIB == 4) || (ib < F::NIB);
-  const bool own = (F::NKT == 8) || (wave < F::NKT);
-  const int ibc = min(ib, F::NIB - 1);
-  const int nks = min(ibc / 2 + 1, F::KS);  // P fragments on or below the diagonal, as T'
-  const int tb = 16 * ibc + 4 * g4;
-  const uint32_t foff = (uint32_t)(((ibc * F::KS) * 64 + lane) * 16);
-  const uint32_t qoff = (uint32_t)(((ibc * F::DS) * 64 + lane) * 16);
-  auto p_res = [&](int lc) {
-    return make_rsrc(pfrag + ((c0 + lc) * hv + h) * F::FRAG, F::FRAG * 2);
-  };
-  auto q_res = [&](int lc) {
-    return make_rsrc(qfrag + ((c0 + lc) * hqk + hk) * (C * D), C * D * 2);
-  };
-  // O of chunk lc from the kept Q S^T, P and the U of that chunk in LDS,
-  // straight to global memory: lane (l16, g4) element e is row tb + e,
-  // column v0 + l16.
-  auto out = [&](const uint4 *pa, const f32x4 &qs, const float *gq, int lc) {
-    uint4 bu[F::KS];
-#pragma unroll
-    for (int s = 0; s < F::KS; ++s)
-      bu[s] = *reinterpret_cast<const uint4 *>(&L.Ul[l16 * F::LDV + 32 * s + 8 * g4]);
-    __builtin_amdgcn_sched_barrier(0);
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < F::KS; ++s) acc = mfma_16x16x32(pa[s], bu[s], acc);
-    const int64_t t0 = seq_t0 + (int64_t)lc * C;
-    const int nv = (int)min((int64_t)C, seq_t1 - t0);
-    const rsrc_t ro = make_rsrc(o + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * CC::ESZ));
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      BufElem<TIn>::store1_stream(ro, (uint32_t)((tb + e) * hv * D + l16), gq[e] * qs[e] + acc[e]);
-  };
-  uint4 qf[F::DS];   // Q rows of block ib, one chunk ahead
-  uint4 pa[F::KS];   // P rows of block ib of the previous chunk
-  uint4 kt[F::KS];   // K^T operands of key tile `wave`
-  f32x4 qs = f32x4{0.f, 0.f, 0.f, 0.f};
-  float gq[4] = {0.f, 0.f, 0.f, 0.f};
-  {
-    const rsrc_t rq = q_res(0);
-#pragma unroll
-    for (int s = 0; s < F::DS; ++s) qf[s] = buf_load_b128(rq, qoff + 1024u * s);
-#pragma unroll
-    for (int s = 0; s < F::KS; ++s) pa[s] = make_uint4(0, 0, 0, 0);
-  }
-  for (int lc = 0; lc < nch; ++lc) {
-    const int b = lc % CC::NB;  // input buffer of chunk lc
-    // ---- phase 1: output of chunk lc - 1, then P of this chunk and the K^T
-    // operands of the state update
-    if (blk) {
-      if (lc > 0) out(pa, qs, gq, lc - 1);
-      __builtin_amdgcn_sched_barrier(0);
-      const rsrc_t rp = p_res(lc);
-#pragma unroll
-      for (int s = 0; s < F::KS; ++s) pa[s] = buf_load_b128(rp, s < nks ? foff + 1024u * s : kOutOfRange);
-    }
-    if (own) {
-#pragma unroll
-      for (int s = 0; s < F::KS; ++s) kt[s] = kt_operand<D>(L.Kn[b], wave, s, l16, g4);
-      // these waves write nothing to LDS in phase 1: the K^T reads may stay
-      // in flight across the barrier
-      lds_barrier_keep<((F::NKT == 8) ? 2 * F::KS : 0)>();
-    } else {
-      lds_barrier();
-    }
-    // ---- phase 2: Q S^T (S is still the state entering chunk lc)
-    if (blk) {
-      uint4 bs[F::DS];
-#pragma unroll
-      for (int s = 0; s < F::DS; ++s)
-        bs[s] = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
-      __builtin_amdgcn_sched_barrier(0);
-      f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < F::DS; ++s) x = mfma_16x16x32(qf[s], bs[s], x);
-      qs = x;
-      const float4 g4v = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
-      gq[0] = g4v.x; gq[1] = g4v.y; gq[2] = g4v.z; gq[3] = g4v.w;
-      // the product must be complete before the registers of Q are reloaded
-      asm volatile("" ::"v"(x) : "memory");
-      const rsrc_t rq = q_res(min(lc + 1, nch - 1));
-#pragma unroll
-      for (int s = 0; s < F::DS; ++s) qf[s] = buf_load_b128(rq, qoff + 1024u * s);
-    }
-    lds_barrier();
-    // ---- phase 3
-    if (own) state_update<D, C, TIn>(L, S, kt, L.Dl[b][C - 1], wave, l16, g4);
-    lds_barrier();
-  }
-  if (blk) out(pa, qs, gq, nch - 1);  // output of the last chunk
-}
-
-template <int D, int C, typename TIn>
-__global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
-    const TIn *__restrict__ k, const TIn *__restrict__ v,
-    const int32_t *__restrict__ cu, const float *__restrict__ dec_ws,
-    const uint16_t *__restrict__ tfrag, const uint16_t *__restrict__ pfrag,
-    const uint16_t *__restrict__ qfrag, const uint16_t *__restrict__ kcopy,
-    const float *s0, float *sT, TIn *__restrict__ o, int hqk, int hv, int group,
-    int n_groups) {
-  using F = Cfg<D, C>;
-  using CC = CarryCfg<D, C, TIn>;
-  __shared__ __attribute__((aligned(16))) CarryLds<D, C, TIn> L;
-
-  // Work-groups are dealt to the 8 XCDs round-robin by id. Give each XCD
-  // whole (sequence, key head) groups, every value head of the group with
-  // all its value tiles, so the tiles that share K and Q (the group) and T'
-  // and P (one head) share one L2.
-  const int Lb = blockIdx.x;
-  const int jx = Lb >> 3;  // index among the work-groups of XCD Lb % 8
-  const int gq = (jx / (group * F::NVT)) * 8 + (Lb & 7);  // sequence * hqk + key head
-  const int gi = (jx / F::NVT) % group, vt = jx % F::NVT;
-  if (gq >= n_groups) return;
-  const int n = gq / hqk, hk = gq % hqk, h = hk * group + gi;
-  const int pair = n * hv + h;
-  const int v0 = 16 * vt;
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int l16 = lane & 15, g4 = lane >> 4;
-  const int64_t seq_t0 = cu[n], seq_t1 = cu[n + 1];
-  const int nch = (int)((seq_t1 - seq_t0 + C - 1) / C);
-  const int64_t c0 = first_slot(cu, n, C);
-  const bool compute = wave < CC::NCW;
-  const bool own = compute && ((F::NKT == 8) || (wave < F::NKT));
-
-  // State rows v0..v0+15, key tile `wave`: lane l holds
-  // S[v0 + l%16][16 wave + 4 (l/16) + e] (the accumulator layout of the
-  // S^T update).
-  f32x4 S = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (own && s0 != nullptr) {
-    const float4 x = *reinterpret_cast<const float4 *>(
-        s0 + ((int64_t)pair * D + v0 + l16) * D + 16 * wave + 4 * g4);
-    S = f32x4{x.x, x.y, x.z, x.w};
-  }
-  if (nch > 0) {  // uniform over the work-group
-    if (compute) {
-      if (C < F::CP) {  // zero the token positions past the chunk, once
-        for (int idx = tid; idx < 16 * F::LDV; idx += 64 * CC::NCW) {
-          L.Yl[idx] = 0;
-          L.Ul[idx] = 0;
-          L.Uh[idx] = 0;
-        }
-        for (int idx = C * D + tid; idx < F::CP * D; idx += 64 * CC::NCW) {
-#pragma unroll
-          for (int bb = 0; bb < CC::NB; ++bb) L.Kn[bb][idx] = 0;
-        }
-      }
-      if (own)
-        *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
-            pack4_bf16(S[0], S[1], S[2], S[3]);
-      lds_barrier();
-      if (wave < 4)
-        carry_compute_xu<D, C, TIn>(L, S, wave, lane, nch, c0, tfrag, h, hv);
-      else
-        carry_compute_o<D, C, TIn>(L, S, wave, lane, nch, c0, pfrag, qfrag, o, seq_t0, seq_t1,
-                                   h, hk, hqk, hv, v0);
-    } else {
-      // bf16 K is copied straight from the input; f32 K from its bf16 copy.
-      const bool kcopied = sizeof(TIn) != 2;
-      const uint16_t *ksrc = kcopied ? kcopy : reinterpret_cast<const uint16_t *>(k);
-      const int kstride = kcopied ? D : hqk * D;
-      static_assert(CC::NLW == 2, "loader dispatch below");
-      if (wave == CC::NCW)
-        carry_loader<D, C, TIn, 0>(L, lane, ksrc, kstride, kcopied, v, dec_ws, nch, seq_t0,
-                                   seq_t1, c0, h, hk, hqk, hv, v0);
-      else
-        carry_loader<D, C, TIn, 1>(L, lane, ksrc, kstride, kcopied, v, dec_ws, nch, seq_t0,
-                                   seq_t1, c0, h, hk, hqk, hv, v0);
-    }
-  }
-
-  if (own)
-    store_stream(sT + ((int64_t)pair * D + v0 + l16) * D + 16 * wave + 4 * g4, S);
-}
-
 // ============================================================ single-wave carry
 // The carry for batches of short sequences: one wavefront per (sequence,
 // value head, 16-row value tile), 4 independent wavefronts per work-group,
@@ -1041,34 +453,6 @@ struct WaveCfg {
   static constexpr int NKI = C * D / 512;  // 1 KB copies per K chunk
 };
 
-// T' (and P) fragments of block row ib that are not all zero: steps s <= ib/2.
-template <int C>
-__device__ __forceinline__ constexpr int frag_steps(int ib) {
-  return (ib / 2 + 1) < (C + 31) / 32 ? (ib / 2 + 1) : (C + 31) / 32;
-}
-
-// B operand of a contraction over the chunk's tokens, step st: blocks 2 st
-// (slots 0-3) and 2 st + 1 (slots 4-7) of accumulator tiles X, each element
-// times w[block][e] (or as is when w is null), rounded to bf16.
-template <int NIB>
-__device__ __forceinline__ uint4 u_operand(const f32x4 (&X)[NIB], int st, const f32x4 *w) {
-  const int b0 = 2 * st, b1 = 2 * st + 1;
-  f32x4 lo = X[b0 % NIB], hi = (b1 < NIB) ? X[b1 % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
-  if (w != nullptr) {
-    lo = lo * w[b0 % NIB];
-    if (b1 < NIB) hi = hi * w[b1 % NIB];
-  }
-  return make_uint4(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]),
-                    pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]));
-}
-
-// 16 x 32 A operand of a key contraction, rows from a row-major matrix:
-// lane (l16, g4) gives row l16, keys 32 s + 4 g4 + [0, 4) and
-// 32 s + 16 + 4 g4 + [0, 4).
-__device__ __forceinline__ uint4 key_operand(uint2 lo, uint2 hi) {
-  return make_uint4(lo.x, lo.y, hi.x, hi.y);
-}
-
 template <int D, int C, typename TIn>
 __global__ __launch_bounds__(256) void chunk_wave_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k, const TIn *__restrict__ v,
@@ -1078,7 +462,6 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
     int n_units, int hqk, int hv, int group) {
   using F = Cfg<D, C>;
   using WC = WaveCfg<D, C>;
-  using CC = CarryCfg<D, C, TIn>;
   constexpr int NIB = F::NIB, KS = F::KS, DS = F::DS, NKT = F::NKT, NVT = F::NVT;
   __shared__ __attribute__((aligned(16))) uint16_t Kw[WC::WAVES][F::CP * D];
 
@@ -1132,7 +515,7 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
     for (int m = 0; m < WC::NKI; ++m) {
       // (the offset goes in as a plain scalar: with an array element as the
       // builtin's argument the host pass emitted no launch stub)
-      const uint32_t off = copy_offset<D, C, TIn>(m, lane, kstride, hv);
+      const uint32_t off = tile_copy_offset<D>(m, lane, kstride);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void *)(K + 512 * m), 16, off, 0, 0, 0);
     }
     const rsrc_t rt = make_rsrc(tfrag + slot * F::FRAG, F::FRAG * 2);
@@ -1273,8 +656,19 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
 // ============================================================ host side
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+int chain_segment_chunks(int64_t n_tokens, int hv, int chunk, int requested) {
+  if (requested > 0) return requested;
+  const int64_t nck = (n_tokens + chunk - 1) / chunk;  // chunks of the longest possible chain
+  const int64_t l = (nck * hv + kChainUnits - 1) / kChainUnits;
+  return (int)std::min<int64_t>(std::max<int64_t>(l, kMinSegmentChunks), 1 << 20);
+}
+
+bool uses_tile_carry(int n_seqs, int hv, int d) {
+  return (int64_t)n_seqs * hv * (d / 16) <= kTileCarryMaxTiles;
+}
+
 PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
-                                          int hv, int d, int chunk) {
+                                          int hv, int d, int chunk, int seg_chunks, bool tile) {
   PrefillWorkspace w;
   const int64_t nc = chunk_bound(n_seqs, n_tokens, chunk);
   size_t p = 0;
@@ -1284,10 +678,22 @@ PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
   p = align256(p + sizeof(uint16_t) * (size_t)nc * hv * frag_elems(chunk));
   w.pfrag = p;
   p = align256(p + sizeof(uint16_t) * (size_t)nc * hv * frag_elems(chunk));
+  const bool wave = uses_wave_carry(n_seqs, n_tokens, chunk);
   w.qfrag = p;
-  p = align256(p + sizeof(uint16_t) * (size_t)nc * hqk * chunk * d);
+  if (tile && !wave) p = align256(p + sizeof(uint16_t) * (size_t)nc * hqk * chunk * d);
   w.kcopy = p;
   p = align256(p + sizeof(uint16_t) * (size_t)nc * hqk * chunk * d);
+  // Maps of every segment but the last of each sequence (whole-chain carry):
+  // at most T / span slots, and none when every sequence fits in one segment.
+  const int64_t span = (int64_t)chunk * seg_chunks;
+  w.n_maps = (!wave && !tile && span < n_tokens) ? n_tokens / span : 0;
+  const size_t mbytes = (size_t)w.n_maps * hv * d * d;
+  w.bslot = p;
+  p = align256(p + sizeof(float) * mbytes);
+  w.mthi = p;
+  p = align256(p + sizeof(uint16_t) * mbytes);
+  w.mtlo = p;
+  p = align256(p + sizeof(uint16_t) * mbytes);
   w.total = p;
   return w;
 }
@@ -1299,8 +705,9 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
   float *dec = reinterpret_cast<float *>(base + ws.decay);
   uint16_t *tf = reinterpret_cast<uint16_t *>(base + ws.tfrag);
   uint16_t *pf = reinterpret_cast<uint16_t *>(base + ws.pfrag);
-  uint16_t *qf = reinterpret_cast<uint16_t *>(base + ws.qfrag);
   uint16_t *kc = reinterpret_cast<uint16_t *>(base + ws.kcopy);
+  uint16_t *qf = (sizeof(TIn) == 2 && a.tile_carry && !a.wave_carry)
+                     ? reinterpret_cast<uint16_t *>(base + ws.qfrag) : nullptr;
   const int group = a.hv / a.hqk;
 
   const int64_t nc = chunk_bound(a.n_seqs, a.n_tokens, C);
@@ -1310,28 +717,26 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
     const int64_t lblocks = ((pairs + 7) / 8) * 8 * group;
     auto local = a.neumann ? chunk_local_kernel<D, C, TIn, true>
                            : chunk_local_kernel<D, C, TIn, false>;
-    hipLaunchKernelGGL(local, dim3((unsigned)lblocks), dim3(256), 0, a.stream, (const TIn *)a.q, (const TIn *)a.k, a.g, a.beta, a.gate,
-                       a.cu_seqlens, a.n_seqs, a.hqk, a.hv, group, (int)pairs, dec, tf, pf,
-                       qf, kc);
+    hipLaunchKernelGGL(local, dim3((unsigned)lblocks), dim3(256), 0, a.stream, (const TIn *)a.q,
+                       (const TIn *)a.k, a.g, a.beta, a.gate, a.cu_seqlens, a.n_seqs, a.hqk, a.hv,
+                       group, (int)pairs, dec, tf, pf, qf, kc);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
 
+  // bf16 inputs: the per-tile carry for few chains, else the whole-chain
+  // carry, unless the average sequence fits in one chunk. f32 inputs (and
+  // short sequences): the single-wave carry, which walks sequences of any
+  // length.
+  if (sizeof(TIn) == 2 && !a.wave_carry)
+    return a.tile_carry ? launch_tile_carry(a, ws) : launch_chain_d(a, ws);
   const int n_groups = a.n_seqs * a.hqk;
-  if (a.wave_carry) {
-    const int wpu = (group * F::NVT + WaveCfg<D, C>::WAVES - 1) / WaveCfg<D, C>::WAVES;
-    const int64_t wblocks = (int64_t)8 * ((n_groups + 7) / 8) * wpu;
-    hipLaunchKernelGGL((chunk_wave_kernel<D, C, TIn>), dim3((unsigned)wblocks), dim3(256), 0,
-                       a.stream, (const TIn *)a.q, (const TIn *)a.k, (const TIn *)a.v,
-                       a.cu_seqlens, dec, tf, pf, kc, a.initial_state, a.final_state, (TIn *)a.o,
-                       n_groups, a.hqk, a.hv, group);
-    return hipGetLastError();
-  }
-  const int64_t blocks = (int64_t)8 * ((n_groups + 7) / 8) * group * F::NVT;
-  hipLaunchKernelGGL((chunk_carry_kernel<D, C, TIn>), dim3((unsigned)blocks),
-                     dim3(kCarryThreads), 0, a.stream, (const TIn *)a.k, (const TIn *)a.v,
-                     a.cu_seqlens, dec, tf, pf, qf, kc, a.initial_state, a.final_state,
-                     (TIn *)a.o, a.hqk, a.hv, group, n_groups);
+  const int wpu = (group * F::NVT + WaveCfg<D, C>::WAVES - 1) / WaveCfg<D, C>::WAVES;
+  const int64_t wblocks = (int64_t)8 * ((n_groups + 7) / 8) * wpu;
+  hipLaunchKernelGGL((chunk_wave_kernel<D, C, TIn>), dim3((unsigned)wblocks), dim3(256), 0,
+                     a.stream, (const TIn *)a.q, (const TIn *)a.k, (const TIn *)a.v,
+                     a.cu_seqlens, dec, tf, pf, kc, a.initial_state, a.final_state, (TIn *)a.o,
+                     n_groups, a.hqk, a.hv, group);
   return hipGetLastError();
 }
 

@@ -11,8 +11,8 @@
 // so every state element is read once and written once per call, whatever the
 // length, and no workspace is touched. Each token costs 6 d^2 vector-ALU
 // flops per head, against matrix-core work in the chunked form, so this path
-// pays only for sequences of a few tokens: the narrow short-shape path of the
-// paper's Section 5.2, chosen by the measured dispatch in gdn_api.hip.
+// pays only for sequences of a few tokens: the narrow short-shape fallback of
+// the paper's Sections 5.3 and 5.5, chosen by the measured dispatch in gdn_api.hip.
 //
 // Launch shape as in the decode kernel: a state row of D fp32 values is held
 // by D/4 lanes, 16 bytes each; a wavefront holds PASSES such row groups of one

@@ -29,6 +29,18 @@ CHUNK_AUTO, CHUNK_SERIAL = 0, 1
 # OR-ed into a chunk size of 16, 32 or 64: diagonal blocks of the WY factor by
 # the Neumann product instead of forward substitution.
 CHUNK_NEUMANN = 0x100
+# OR-ed into a chunk size of 0, 16, 32 or 64: the per-tile carry (instead of
+# the library's choice between it and the whole-chain carry).
+CHUNK_TILE_CARRY = 0x200
+CHUNK_SEGMENT_SHIFT = 16
+
+
+def CHUNK_SEGMENT(n_chunks: int) -> int:
+    """OR-ed into a chunk size of 0, 16, 32 or 64: the whole-chain carry with
+    segments of `n_chunks` chunks (1..4095) instead of the library's choice."""
+    if not 1 <= n_chunks <= 4095:
+        raise ValueError("segment length must be in [1, 4095] chunks")
+    return n_chunks << CHUNK_SEGMENT_SHIFT
 
 _lib = None
 

@@ -43,3 +43,37 @@ def chain_slice(x: dict, n: int, h: int):
                 beta=x["beta"][t0:t1, h:h + 1],
                 cu_seqlens=np.array([0, t1 - t0], np.int32),
                 initial_state=None if s0 is None else s0[n:n + 1, h:h + 1])
+
+
+def chain_errors(o, sT, o_ref, s_ref, cu):
+    """Whole-tensor and per-(sequence, value head) rel-L2 of a prefill result.
+
+    o, o_ref: [T, HV, DV]; sT, s_ref: [N, HV, DV, DK]; cu: cu_seqlens.
+    Returns dict(o=, state=, o_max=, state_max=, worst=(n, h)) where o_max and
+    state_max are the largest per-chain errors (sequences of length 0 count
+    only for the state).
+    """
+    o = _np(o)
+    sT = _np(sT)
+    o_ref = np.asarray(o_ref, dtype=np.float64)
+    s_ref = np.asarray(s_ref, dtype=np.float64)
+    cu = np.asarray(cu).astype(np.int64)
+    N, HV = s_ref.shape[0], s_ref.shape[1]
+    o_max = s_max = 0.0
+    worst = (-1, -1)
+    for n in range(N):
+        t0, t1 = cu[n], cu[n + 1]
+        for h in range(HV):
+            es = rel_l2(sT[n, h], s_ref[n, h])
+            eo = rel_l2(o[t0:t1, h], o_ref[t0:t1, h]) if t1 > t0 else 0.0
+            if max(eo / 2e-2, es / 5e-3) > max(o_max / 2e-2, s_max / 5e-3):
+                worst = (n, h)
+            o_max, s_max = max(o_max, eo), max(s_max, es)
+    return dict(o=rel_l2(o, o_ref), state=rel_l2(sT, s_ref), o_max=o_max,
+                state_max=s_max, worst=worst)
+
+
+def _np(x):
+    if hasattr(x, "detach"):
+        return x.detach().cpu().double().numpy()
+    return np.asarray(x, dtype=np.float64)

@@ -213,3 +213,38 @@ def test_binding_refuses_host_tensors():
     with pytest.raises(ValueError):
         gdn.decode(x, x, x, torch.zeros(4, 1), torch.zeros(4, 1),
                    torch.zeros(4, 1, 32, 32), o=torch.zeros(4, 1, 32))
+
+
+def test_carry_flags_sizes_and_validation():
+    """The carry choice and GDN_CHUNK_SEGMENT(L). The 4096-token workload (one
+    sequence, 16/32 heads, C = 64: 256 value tiles) takes the per-tile carry,
+    whose workspace adds the Q fragment table and holds no segment maps; the
+    66K-token batch of 16 sequences takes the whole-chain carry. With a forced
+    segment length the workspace grows as segments shrink (more maps) and has
+    no maps when one segment holds every sequence. Refused: a flag with
+    chunk = 1, the tile flag together with a segment length, unknown bits."""
+    ws = gdn.prefill_workspace_size
+    S = gdn.CHUNK_SEGMENT
+    TILE = gdn.CHUNK_TILE_CARRY
+    auto = ws(1, 4096, 16, 32, 128, 128, 64)
+    assert auto == ws(1, 4096, 16, 32, 128, 128, 64 | TILE)
+    one = ws(1, 4096, 16, 32, 128, 128, 64 | S(64))
+    # Q fragments: (64 + 1 chunk slots) x 16 key heads x 64 x 128 bf16
+    assert auto - one == 65 * 16 * 64 * 128 * 2
+    eight = ws(1, 4096, 16, 32, 128, 128, 64 | S(8))
+    # 8 segments -> 7 maps, each B (fp32) + M^T hi/lo (bf16): 8 * 32 * 128 * 128 * 8 bytes
+    assert eight - one == 8 * 32 * 128 * 128 * 8
+    assert ws(1, 4096, 16, 32, 128, 128, 64 | S(4)) > eight
+    assert one == ws(1, 4096, 16, 32, 128, 128, 64 | S(4095))
+    # many chains: the whole-chain carry (no Q fragments), segments picked by size
+    big = ws(16, 66000, 16, 32, 128, 128, 64)
+    assert big < ws(16, 66000, 16, 32, 128, 128, 64 | TILE)
+    for bad in (1 | S(2), 1 | TILE, 64 | TILE | S(2), 64 | (1 << 30)):
+        assert ws(1, 4096, 16, 32, 128, 128, bad) == 0
+        assert _prefill(chunk=bad) == gdn.GDN_ERR_UNSUPPORTED
+    assert ws(1, 4096, 16, 32, 128, 128, 0 | S(2)) >= ws(1, 4096, 16, 32, 128, 128, 64 | S(2))
+    with pytest.raises(ValueError):
+        S(0)
+    with pytest.raises(ValueError):
+        S(4096)
+    assert _prefill(chunk=64 | S(2), workspace_bytes=0) == gdn.GDN_ERR_WORKSPACE
