@@ -28,7 +28,6 @@ import glob
 import hashlib
 import json
 import os
-import platform
 import sys
 import time
 
@@ -63,6 +62,27 @@ def kernel_source_hash():
 
 def prefill_flops(T, hqk, hv, d, C):
     return float(T) * hv * (6 * d * d + (6 + 4.0 * hqk / hv) * C * d + C * C / 3.0)
+
+
+def prefill_flops_executed(T, hqk, hv, d, C):
+    """Products the kernels run in the R form (U = T'(V - exp(gamma) K S^T),
+    no W = T'(beta Gamma K)): 6 d^2 (K S^T, Q S^T, the state update) +
+    4 C d (T' Y and P U) + 4 (HQK/HV) C d (the two Gram products, shared by
+    a key head's value heads) + C^2/3 (the triangular factor) per token and
+    value head. The fixed formula above also counts the W product (2 C d)."""
+    return float(T) * hv * (6 * d * d + (4 + 4.0 * hqk / hv) * C * d + C * C / 3.0)
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or platform.machine()
 
 
 def prefill_bytes(T, N, hqk, hv, d, e, has_s0):
@@ -166,6 +186,21 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
 
+    # The same K prefill calls with a workspace per input set: the per-chunk
+    # tables then never land on lines the previous call left in the caches.
+    wss = [P[0]["ws"]] + [torch.empty_like(P[0]["ws"]) for _ in range(1, args.rotate)]
+    for i in range(args.rotate):
+        run_prefill(dict(P[i], ws=wss[i]))
+    torch.cuda.synchronize()
+    ec = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ec[0].record()
+    for i in range(K):
+        run_prefill(dict(P[i % args.rotate], ws=wss[i % args.rotate]))
+    ec[1].record()
+    torch.cuda.synchronize()
+    pre_cold_avg = ec[0].elapsed_time(ec[1]) / 1e3 / K
+    del wss
+
     pre_s = ev[0].elapsed_time(ev[1]) / 1e3
     dec_s = ev[1].elapsed_time(ev[2]) / 1e3
     T = P[0]["q"].shape[0]
@@ -173,6 +208,7 @@ def main():
     dec_avg = dec_s / K
     pre_tps = K * T / pre_s
     flop = prefill_flops(T, wp.hqk, wp.hv, wp.d, wp.chunk)
+    flop_exec = prefill_flops_executed(T, wp.hqk, wp.hv, wp.d, wp.chunk)
     pbytes = prefill_bytes(T, wp.n_seqs, wp.hqk, wp.hv, wp.d, 2, False)
     dbytes = decode_bytes(wd.n_seqs, wd.hqk, wd.hv, wd.d)
     pre_tflops = flop / pre_avg / 1e12
@@ -185,6 +221,8 @@ def main():
                 "traffic": measured["prefill"] if measured else None,
                 "kernel": "gdn_prefill (chunk_local + chunk_carry)",
                 "algorithmic_flop_per_launch": flop,
+                "executed_flop_per_launch": flop_exec,
+                "frac_executed": round(flop_exec / pre_avg / 1e12 / PEAK_BF16_TFLOPS, 4),
                 "hbm_view_gbs": round(pbytes / pre_avg / 1e9, 1)}
     roof_dec = {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(dec_gbs / PEAK_HBM_GBS, 4),
@@ -203,6 +241,7 @@ def main():
                    "heads_qk_v": [wp.hqk, wp.hv], "d": wp.d, "chunk": wp.chunk,
                    "rotating_input_sets": args.rotate},
         "prefill": {"us_per_call": round(pre_avg * 1e6, 2),
+                    "us_per_call_workspace_per_set": round(pre_cold_avg * 1e6, 2),
                     "tokens_per_s": round(pre_tps, 1), "tflops": round(pre_tflops, 2),
                     "mfma_util": round(pre_tflops / PEAK_BF16_TFLOPS, 4)},
         "decode": {"us_per_step": round(dec_avg * 1e6, 2),
@@ -212,35 +251,51 @@ def main():
     }
 
     # ---------------------------------------------------- small-batch decode
-    # Latency of one decode step per batch size (same heads and d): K steps
-    # are captured in a HIP graph and replayed, so the time per step is the
-    # kernel's, without the host launch path of the Python binding.
+    # Latency of one decode step per batch size (same heads and d), from cold
+    # state: each step advances a different state buffer, rotating over
+    # enough buffers (at least 3, and at least 3 x 256 MiB in all) that the
+    # Infinity Cache cannot hold the state between its visits. The steps are
+    # captured in a HIP graph and replayed, so the time per step is the
+    # kernel's, without the host launch path of the Python binding. The warm
+    # figure (one state buffer, 20 steps) rides alongside.
     if not args.no_decode_sweep:
-        lat = {}
+        lat, warm, cold_frac = {}, {}, {}
         for B in (1, 8, 16, 48, 64):
             w = wd.replace(n_seqs=B, seed=wd.seed + 7)
             y = synth.make(w)
             t = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in y.items()}
             t["o"] = torch.empty((B, w.hv, w.d), dtype=torch.bfloat16, device=dev)
-            for _ in range(3):
-                run_decode(t)
-            torch.cuda.synchronize()
-            graph, KG = torch.cuda.CUDAGraph(), 20
-            with torch.cuda.graph(graph):
-                for _ in range(KG):
-                    run_decode(t)
-            graph.replay()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            R = 5
-            e0.record()
-            for _ in range(R):
+            sbytes = t["initial_state"].numel() * 4
+            nset = max(3, -(-3 * (256 << 20) // sbytes))
+            states = [t["initial_state"].clone() for _ in range(nset)]
+
+            def graph_time(sts, reps):
+                for st in sts[:3]:
+                    run_decode(dict(t, initial_state=st))
+                torch.cuda.synchronize()
+                graph = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(graph):
+                    for st in sts:
+                        run_decode(dict(t, initial_state=st))
                 graph.replay()
-            e1.record()
-            torch.cuda.synchronize()
-            lat[str(B)] = round(e0.elapsed_time(e1) * 1e3 / (R * KG), 2)
-            del graph
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(reps):
+                    graph.replay()
+                e1.record()
+                torch.cuda.synchronize()
+                del graph
+                return e0.elapsed_time(e1) * 1e3 / (reps * len(sts))
+
+            lat[str(B)] = round(graph_time(states, 3), 2)
+            warm[str(B)] = round(graph_time([t["initial_state"]] * 20, 5), 2)
+            cold_frac[str(B)] = round(decode_bytes(B, w.hqk, w.hv, w.d) / (lat[str(B)] * 1e-6)
+                                      / 1e9 / PEAK_HBM_GBS, 4)
+            del states, t
         out["decode_latency_us"] = lat
+        out["decode_latency_hbm_frac"] = cold_frac
+        out["decode_latency_warm_us"] = warm
 
     # ------------------------------------------------- prefill shape dispatch
     # Batches of N equal-length sequences (same heads, d and dtype as the
@@ -293,7 +348,9 @@ def main():
             "value": round(reps * T / el, 1), "unit": "tokens/s",
             "cores": oracle.num_threads(), "kind": "oracle",
             "sample": "%d full runs of the 4096-token prefill (all 32 heads), fp64 "
-                      "token-serial, %.1f s wall on %s" % (reps, el, platform.processor() or platform.machine())}
+                      "token-serial, %.1f s wall on %d threads of %s (%d logical CPUs)"
+                      % (reps, el, oracle.num_threads(), cpu_model(), os.cpu_count() or 0),
+            "cpu_model": cpu_model()}
     print(json.dumps(out), flush=True)
 
 

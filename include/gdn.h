@@ -145,6 +145,20 @@ int32_t gdn_prefill_auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hqk,
  * unit lower-triangular WY factor; the state is carried chunk to chunk in
  * float32.
  *
+ * The carry from chunk to chunk takes one of two forms, chosen from the
+ * sizes unless GDN_CHUNK_TILE_CARRY or GDN_CHUNK_SEGMENT(L) forces one: with
+ * fewer than 256 (sequence, value head) chains, the per-tile carry spreads
+ * every chain over DV/16 work-groups of 16 value rows; with more, the
+ * whole-chain carry gives each chain (or each segment of a long chain,
+ * joined through the segments' affine state maps) one work-group. Batches
+ * whose average sequence fits in one chunk use a third, single-wavefront
+ * carry. All three give the same result up to rounding.
+ *
+ * Precision of the chunked path: bf16 inputs enter the matrix products as
+ * bf16 operands with float32 accumulation, and the state is carried in
+ * float32 (rel-L2 against an fp64 evaluation of the recurrence about 2e-3
+ * to 4e-3 on o and the final state at the benchmark sizes).
+ *
  * chunk = 1 runs the token-serial form instead: the recurrence token by
  * token in float32 on the vector ALU, the state held in registers for the
  * whole sequence (the narrow short-shape fallback, paper Sections 5.3 and 5.5). chunk = 0 picks

@@ -73,9 +73,13 @@ inline int64_t chunk_bound(int n_seqs, int64_t n_tokens, int chunk) {
 // Chunks per segment of the whole-chain carry: `requested` if positive, else
 // enough that the segments of all chains give about kChainUnits work-groups.
 constexpr int kChainUnits = 256;
-// Largest number of 16-row value tiles (sequences x value heads x D/16) for
-// which the per-tile carry is chosen.
-constexpr int64_t kTileCarryMaxTiles = 256;
+// The whole-chain carry needs at least this many (sequence, value head)
+// chains, one work-group each, to fill the chip; with fewer the per-tile
+// carry spreads every chain over D/16 work-groups instead. Measured on the
+// 66K-token batch of 16 sequences (512 chains: whole-chain 1.20 ms, per-tile
+// 1.44 ms) and on 2 x 32768 tokens (64 chains: per-tile 1.47 ms, whole-chain
+// with segments 1.54 ms).
+constexpr int64_t kChainCarryMinChains = 256;
 constexpr int kMinSegmentChunks = 4;
 int chain_segment_chunks(int64_t n_tokens, int hv, int chunk, int requested);
 // The whole-chain carry runs unless the average sequence fits in one chunk
@@ -83,8 +87,9 @@ int chain_segment_chunks(int64_t n_tokens, int hv, int chunk, int requested);
 inline bool uses_wave_carry(int n_seqs, int64_t n_tokens, int chunk) {
   return n_tokens <= (int64_t)n_seqs * chunk;
 }
-// The per-tile carry when the batch has few (sequence, value head) chains:
-// every chain is then spread over D/16 work-groups without segments.
+// The per-tile carry when the batch has fewer (sequence, value head) chains
+// than kChainCarryMinChains: every chain is then spread over D/16
+// work-groups without segments.
 bool uses_tile_carry(int n_seqs, int hv, int d);
 PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
                                           int hv, int d, int chunk, int seg_chunks, bool tile);

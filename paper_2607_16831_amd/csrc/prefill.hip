@@ -663,8 +663,8 @@ int chain_segment_chunks(int64_t n_tokens, int hv, int chunk, int requested) {
   return (int)std::min<int64_t>(std::max<int64_t>(l, kMinSegmentChunks), 1 << 20);
 }
 
-bool uses_tile_carry(int n_seqs, int hv, int d) {
-  return (int64_t)n_seqs * hv * (d / 16) <= kTileCarryMaxTiles;
+bool uses_tile_carry(int n_seqs, int hv, int) {
+  return (int64_t)n_seqs * hv < kChainCarryMinChains;
 }
 
 PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,

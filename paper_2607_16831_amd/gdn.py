@@ -126,6 +126,40 @@ def _check_dev(*ts):
             raise ValueError("libgdn takes contiguous tensors")
 
 
+def _shape_error(name, t, want):
+    raise ValueError("%s must have shape %s, got %s" % (name, tuple(want), tuple(t.shape)))
+
+
+def _check_shapes(q, k, v, rows, n_states, gates, state_tensors, o):
+    """Every tensor's shape against the sizes taken from q and v, before any
+    launch: the C ABI receives bare pointers and cannot tell a short tensor
+    from a full one, so a wrong shape would make the kernels read or write
+    out of bounds."""
+    if q.dim() != 3:
+        raise ValueError("q must be [tokens, heads_qk, d_k], got %s" % (tuple(q.shape),))
+    if v.dim() != 3:
+        raise ValueError("v must be [tokens, heads_v, d_v], got %s" % (tuple(v.shape),))
+    _, hqk, dk = q.shape
+    hv, dv = v.shape[1], v.shape[2]
+    if tuple(k.shape) != tuple(q.shape):
+        _shape_error("k", k, q.shape)
+    if v.shape[0] != rows:
+        _shape_error("v", v, (rows, hv, dv))
+    for name, t in gates:
+        if t is not None and tuple(t.shape) != (rows, hv):
+            _shape_error(name, t, (rows, hv))
+    for name, t in state_tensors:
+        if t is not None and tuple(t.shape) != (n_states, hv, dv, dk):
+            _shape_error(name, t, (n_states, hv, dv, dk))
+    if o is not None and tuple(o.shape) != (rows, hv, dv):
+        _shape_error("o", o, (rows, hv, dv))
+
+
+def _check_cu(cu_seqlens):
+    if cu_seqlens.dim() != 1 or cu_seqlens.shape[0] < 1:
+        raise ValueError("cu_seqlens must be a 1-D tensor of n_seqs + 1 offsets")
+
+
 def _stream(stream) -> ctypes.c_void_p:
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -184,9 +218,13 @@ def prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor,
     chunk: 16, 32 or 64 (chunked path), CHUNK_SERIAL (token-serial path) or
     CHUNK_AUTO (the library's shape dispatch).
     """
+    _check_cu(cu_seqlens)
+    N = cu_seqlens.shape[0] - 1
+    _check_shapes(q, k, v, q.shape[0] if q.dim() == 3 else -1, N,
+                  (("g", g), ("beta", beta)),
+                  (("initial_state", initial_state), ("final_state", final_state)), o)
     T, hqk, dk = q.shape
     hv, dv = v.shape[1], v.shape[2]
-    N = cu_seqlens.shape[0] - 1
     if o is None:
         o = torch.empty((T, hv, dv), dtype=q.dtype, device=q.device)
     if final_state is None:
@@ -213,6 +251,8 @@ def decode(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor,
            beta: torch.Tensor, state: torch.Tensor,
            o: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """One decode step; advances ``state`` in place and returns o [B, HV, DV]."""
+    B = q.shape[0] if q.dim() == 3 else -1
+    _check_shapes(q, k, v, B, B, (("g", g), ("beta", beta)), (("state", state),), o)
     B, hqk, dk = q.shape
     hv, dv = v.shape[1], v.shape[2]
     if o is None:
@@ -247,9 +287,12 @@ def prefill_gated(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, a: torch.Te
                   workspace: Optional[torch.Tensor] = None,
                   stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Chunked prefill from the raw gate inputs a, b [T, HV], A_log, dt_bias [HV]."""
+    _check_cu(cu_seqlens)
+    N = cu_seqlens.shape[0] - 1
+    _check_shapes(q, k, v, q.shape[0] if q.dim() == 3 else -1, N, (),
+                  (("initial_state", initial_state), ("final_state", final_state)), o)
     T, hqk, dk = q.shape
     hv, dv = v.shape[1], v.shape[2]
-    N = cu_seqlens.shape[0] - 1
     _check_gate(a, b, a_log, dt_bias, T, hv)
     if o is None:
         o = torch.empty((T, hv, dv), dtype=q.dtype, device=q.device)
@@ -277,6 +320,8 @@ def decode_gated(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, a: torch.Ten
                  state: torch.Tensor, o: Optional[torch.Tensor] = None,
                  stream=None) -> torch.Tensor:
     """One decode step from the raw gate inputs; advances ``state`` in place."""
+    B = q.shape[0] if q.dim() == 3 else -1
+    _check_shapes(q, k, v, B, B, (), (("state", state),), o)
     B, hqk, dk = q.shape
     hv, dv = v.shape[1], v.shape[2]
     _check_gate(a, b, a_log, dt_bias, B, hv)

@@ -18,8 +18,10 @@ contest's 54 decode and 100 prefill workloads):
 * raw gate inputs (workloads with raw_gate): a, b ~ N(0, 1) per (token, head),
   A_log = log(A) with A ~ U(1, 16) per head, and dt_bias the inverse softplus
   of dt = exp(U(log 0.001, log 0.1)) per head -- the usual initialisation of
-  these parameters in gated linear-attention layers; g and beta are then
-  formed from them in fp32 (the kernels form their own).
+  these parameters in gated linear-attention layers. Such a workload carries
+  no g and beta: the gate activation is part of the method, so only its
+  implementations form them (the kernels, and the oracle's gate for the
+  tests).
 * q, k, v are produced in fp32 and rounded to bf16 (round to nearest even)
   when the workload is bf16; g, beta and states stay fp32.
 
@@ -110,8 +112,8 @@ def make(w: Workload, seed: Optional[int] = None) -> dict:
     Returns a dict with q, k, v (bf16 or f32), g, beta (f32), cu_seqlens
     (int32), initial_state (f32 or None; for decode the state that is
     advanced in place) and the workload itself under "w". With w.raw_gate it
-    also holds a, b [T, HV] and A_log, dt_bias [HV] (f32), and g, beta are
-    formed from them.
+    holds a, b [T, HV] and A_log, dt_bias [HV] (f32) instead, and g, beta
+    are None.
     """
     gen = torch.Generator().manual_seed(w.seed if seed is None else seed)
     lens = seq_lengths(w, gen)
@@ -143,10 +145,8 @@ def make(w: Workload, seed: Optional[int] = None) -> dict:
         dt = torch.exp(np.log(1e-3) + (np.log(1e-1) - np.log(1e-3)) *
                        torch.rand((w.hv,), generator=gen))
         dt_bias = dt + torch.log(-torch.expm1(-dt))  # softplus(dt_bias) = dt
-        a_log = torch.log(A)
-        g = -torch.exp(a_log) * torch.nn.functional.softplus(a + dt_bias)
-        beta = torch.sigmoid(b)
-        out.update(a=a.contiguous(), b=b.contiguous(), A_log=a_log.contiguous(),
-                   dt_bias=dt_bias.contiguous())
+        out.update(a=a.contiguous(), b=b.contiguous(), A_log=torch.log(A).contiguous(),
+                   dt_bias=dt_bias.contiguous(), g=None, beta=None)
+        return out
     out.update(g=g.float().contiguous(), beta=beta.float().contiguous())
     return out

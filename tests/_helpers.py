@@ -17,6 +17,16 @@ def rel_l2(x, y) -> float:
     return float(np.linalg.norm(x - y) / ny)
 
 
+def gates_from_raw(x: dict):
+    """fp32 g and beta of a raw-gate input set, formed by the oracle's gate
+    activation (fp64, then rounded to fp32): the input of the plain entry
+    points that the gated ones are compared with."""
+    import oracle
+    g, beta = oracle.gate(x["a"], x["b"], x["A_log"], x["dt_bias"])
+    return (torch.from_numpy(g).float().contiguous(),
+            torch.from_numpy(beta).float().contiguous())
+
+
 def require_gpu():
     if not torch.cuda.is_available():
         raise RuntimeError("GPU test run without a visible GPU")
@@ -38,9 +48,10 @@ def chain_slice(x: dict, n: int, h: int):
     t0, t1 = int(cu[n]), int(cu[n + 1])
     hk = h // grp
     s0 = x["initial_state"]
+    g, beta = x["g"], x["beta"]  # None for raw-gate input sets
     return dict(q=x["q"][t0:t1, hk:hk + 1], k=x["k"][t0:t1, hk:hk + 1],
-                v=x["v"][t0:t1, h:h + 1], g=x["g"][t0:t1, h:h + 1],
-                beta=x["beta"][t0:t1, h:h + 1],
+                v=x["v"][t0:t1, h:h + 1], g=None if g is None else g[t0:t1, h:h + 1],
+                beta=None if beta is None else beta[t0:t1, h:h + 1],
                 cu_seqlens=np.array([0, t1 - t0], np.int32),
                 initial_state=None if s0 is None else s0[n:n + 1, h:h + 1])
 

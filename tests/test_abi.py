@@ -217,7 +217,7 @@ def test_binding_refuses_host_tensors():
 
 def test_carry_flags_sizes_and_validation():
     """The carry choice and GDN_CHUNK_SEGMENT(L). The 4096-token workload (one
-    sequence, 16/32 heads, C = 64: 256 value tiles) takes the per-tile carry,
+    sequence, 16/32 heads, C = 64: 32 chains) takes the per-tile carry,
     whose workspace adds the Q fragment table and holds no segment maps; the
     66K-token batch of 16 sequences takes the whole-chain carry. With a forced
     segment length the workspace grows as segments shrink (more maps) and has
@@ -248,3 +248,56 @@ def test_carry_flags_sizes_and_validation():
     with pytest.raises(ValueError):
         S(4096)
     assert _prefill(chunk=64 | S(2), workspace_bytes=0) == gdn.GDN_ERR_WORKSPACE
+
+
+def test_binding_checks_every_shape_before_launch():
+    """The binding compares every tensor with the sizes taken from q and v
+    before it reaches the C ABI (which gets bare pointers): a short state,
+    gate or output tensor raises ValueError naming the tensor, and no call is
+    made. The tensors are host tensors, so a shape that passed would stop at
+    the device check with a different message."""
+    import torch
+    T, N, hqk, hv, d = 12, 2, 1, 2, 32
+    q = torch.zeros(T, hqk, d)
+    v = torch.zeros(T, hv, d)
+    g = torch.zeros(T, hv)
+    cu = torch.tensor([0, 5, 12], dtype=torch.int32)
+    good = dict(q=q, k=q, v=v, g=g, beta=g, cu_seqlens=cu,
+                initial_state=torch.zeros(N, hv, d, d), o=torch.zeros(T, hv, d),
+                final_state=torch.zeros(N, hv, d, d))
+    with pytest.raises(ValueError, match="device tensors"):
+        gdn.prefill(**good)
+    bad = {
+        "k": torch.zeros(T, hqk + 1, d), "v": torch.zeros(T - 1, hv, d),
+        "g": torch.zeros(T, hv + 1), "beta": torch.zeros(T - 1, hv),
+        "initial_state": torch.zeros(N - 1, hv, d, d),
+        "final_state": torch.zeros(N, hv, d, d - 1), "o": torch.zeros(T, hv, d + 1),
+    }
+    for name, t in bad.items():
+        with pytest.raises(ValueError, match="^%s must have shape" % name):
+            gdn.prefill(**dict(good, **{name: t}))
+    with pytest.raises(ValueError, match="cu_seqlens"):
+        gdn.prefill(**dict(good, cu_seqlens=torch.zeros(0, dtype=torch.int32)))
+
+    B = 3
+    dq, dv = torch.zeros(B, hqk, d), torch.zeros(B, hv, d)
+    dg = torch.zeros(B, hv)
+    dgood = dict(q=dq, k=dq, v=dv, g=dg, beta=dg, state=torch.zeros(B, hv, d, d),
+                 o=torch.zeros(B, hv, d))
+    with pytest.raises(ValueError, match="device tensors"):
+        gdn.decode(**dgood)
+    dbad = {"k": torch.zeros(B, hqk, d + 1), "v": torch.zeros(B + 1, hv, d),
+            "g": torch.zeros(B, hv - 1), "beta": torch.zeros(B + 1, hv),
+            "state": torch.zeros(B - 1, hv, d, d), "o": torch.zeros(B, hv - 1, d)}
+    for name, t in dbad.items():
+        with pytest.raises(ValueError, match="^%s must have shape" % name):
+            gdn.decode(**dict(dgood, **{name: t}))
+
+    # the gated entry points check the same tensors (the gates by their own rule)
+    a = torch.zeros(T, hv)
+    hvec = torch.zeros(hv)
+    with pytest.raises(ValueError, match="^final_state must have shape"):
+        gdn.prefill_gated(q, q, v, a, a, hvec, hvec, cu,
+                          final_state=torch.zeros(N + 1, hv, d, d))
+    with pytest.raises(ValueError, match="^state must have shape"):
+        gdn.decode_gated(dq, dq, dv, dg, dg, hvec, hvec, torch.zeros(B, hv, d, 2 * d))

@@ -4,14 +4,15 @@ gdn_prefill_gated / gdn_decode_gated form g = -exp(A_log) softplus(a +
 dt_bias) and beta = sigmoid(b) in fp32 inside the kernels (paper, Section
 3.2). They are compared with the fp64 oracle run on the same raw inputs (bars
 as for the plain entry points), and with the plain entry points fed g and beta
-formed on the host in fp32 (agreement to fp32 rounding of the gates).
+from the oracle's gate rounded to fp32 (agreement to fp32 rounding of the
+gates).
 """
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from _helpers import O_BAR, STATE_BAR, rel_l2, require_gpu, to_dev
+from _helpers import O_BAR, STATE_BAR, gates_from_raw, rel_l2, require_gpu, to_dev
 from paper_2607_16831_amd import gdn, synth
 
 pytestmark = pytest.mark.gpu
@@ -53,7 +54,8 @@ def test_prefill_gated_matches_plain():
     o1, s1 = gdn.prefill_gated(dd["q"], dd["k"], dd["v"], dd["a"], dd["b"], dd["A_log"],
                                dd["dt_bias"], dd["cu_seqlens"],
                                initial_state=dd["initial_state"], chunk=64)
-    o2, s2 = gdn.prefill(dd["q"], dd["k"], dd["v"], dd["g"], dd["beta"], dd["cu_seqlens"],
+    g, beta = (t.to(dev) for t in gates_from_raw(x))
+    o2, s2 = gdn.prefill(dd["q"], dd["k"], dd["v"], g, beta, dd["cu_seqlens"],
                          initial_state=dd["initial_state"], chunk=64)
     torch.cuda.synchronize()
     eo, es = rel_l2(o1, o2), rel_l2(s1, s2)
@@ -80,7 +82,8 @@ def test_decode_gated_vs_oracle(dtype):
     assert eo <= (O_BAR if dtype == "bf16" else 1e-5) and es <= 1e-5
     # and equal to the plain step on host-formed gates, to fp32 rounding
     state2 = dd["initial_state"].clone()
-    o2 = gdn.decode(dd["q"], dd["k"], dd["v"], dd["g"], dd["beta"], state2)
+    g, beta = (t.to(dev) for t in gates_from_raw(x))
+    o2 = gdn.decode(dd["q"], dd["k"], dd["v"], g, beta, state2)
     torch.cuda.synchronize()
     assert rel_l2(state, state2) <= 1e-6
     assert rel_l2(o.float(), o2.float()) <= (8e-3 if dtype == "bf16" else 1e-6)

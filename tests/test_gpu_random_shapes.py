@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import oracle
-from _helpers import O_BAR, STATE_BAR, rel_l2, require_gpu, to_dev
+from _helpers import O_BAR, STATE_BAR, chain_errors, rel_l2, require_gpu, to_dev
 from paper_2607_16831_amd import gdn, synth
 
 pytestmark = pytest.mark.gpu
@@ -55,14 +55,20 @@ def test_random_configuration(seed):
     serial = chunk == gdn.CHUNK_SERIAL or (
         chunk == gdn.CHUNK_AUTO and
         gdn.prefill_auto_chunk(len(lengths), sum(lengths), hqk, hv, d, d) == gdn.CHUNK_SERIAL)
-    eo = rel_l2(o, o_ref) if o.numel() else 0.0
-    es = rel_l2(sT, s_ref)
-    print("[parity] random%d d=%d heads=%d/%d lengths=%s chunk=%#x %s S0=%s g_mu=%.2f o=%.3e state=%.3e"
-          % (seed, d, hqk, hv, lengths, chunk, dtype, state_std > 0, g_mu, eo, es), flush=True)
+    e = chain_errors(o, sT, o_ref, s_ref, x["cu_seqlens"])
+    eo = e["o"] if o.numel() else 0.0
+    es = e["state"]
+    print("[parity] random%d d=%d heads=%d/%d lengths=%s chunk=%#x %s S0=%s g_mu=%.2f "
+          "o=%.3e state=%.3e o_chain_max=%.3e state_chain_max=%.3e worst=%s"
+          % (seed, d, hqk, hv, lengths, chunk, dtype, state_std > 0, g_mu, eo, es,
+             e["o_max"], e["state_max"], e["worst"]), flush=True)
+    # whole tensor and every (sequence, value head) chain on its own
     if serial:
-        assert eo <= (4e-3 if dtype == "bf16" else 1e-5) and es <= 2e-5
+        ob, sb = (4e-3 if dtype == "bf16" else 1e-5), 2e-5
     else:
-        assert eo <= O_BAR and es <= STATE_BAR
+        ob, sb = O_BAR, STATE_BAR
+    assert eo <= ob and es <= sb
+    assert e["o_max"] <= ob and e["state_max"] <= sb
 
 
 @pytest.mark.parametrize("seed", range(8))

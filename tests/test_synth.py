@@ -62,4 +62,5 @@ def test_raw_gate_draws_leave_other_inputs_alone():
     assert (A >= 1).all() and (A <= 16).all()
     dt = torch.nn.functional.softplus(y["dt_bias"].double())
     assert (dt >= 0.999e-3).all() and (dt <= 0.1001).all()
-    assert (y["g"] < 0).all() and (y["beta"] > 0).all() and (y["beta"] < 1).all()
+    # the gate activation is left to its implementations
+    assert y["g"] is None and y["beta"] is None
