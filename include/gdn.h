@@ -184,6 +184,36 @@ gdn_status gdn_prefill(const void *q, const void *k, const void *v,
                        hipStream_t stream);
 
 /*
+ * gdn_prefill for callers that cannot allocate device memory or pass a
+ * workspace (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation): the same operation, arguments and results as
+ * gdn_prefill, with the workspace taken from a fixed array of
+ * GDN_PREFILL_SCRATCH_MAX_BYTES bytes that the library's code object holds
+ * on each device it runs on until the process ends. The call allocates
+ * nothing. It uses the array of the current device (hipGetDevice), whose
+ * address it looks up on its first call there.
+ *
+ * Sizes whose workspace (gdn_prefill_workspace_size with the same `chunk`)
+ * exceeds GDN_PREFILL_SCRATCH_MAX_BYTES are refused with GDN_ERR_WORKSPACE
+ * before any HIP call; the 128 MiB hold, for example, one 4096-token
+ * sequence with 16 query/key and 32 value heads of size 128 at chunk 64
+ * (66 MiB). Every call on one device shares that device's array: calls that
+ * overlap in time on one device (different streams, or different host
+ * threads without ordering) race and give undefined results; calls ordered
+ * on one stream do not. GDN_ERR_HIP if the array's address cannot be
+ * obtained.
+ */
+#define GDN_PREFILL_SCRATCH_MAX_BYTES (128u << 20)
+
+gdn_status gdn_prefill_scratch(const void *q, const void *k, const void *v,
+                               const float *g, const float *beta,
+                               const int32_t *cu_seqlens, const float *initial_state,
+                               void *o, float *final_state, int32_t n_seqs,
+                               int64_t n_tokens, int32_t hqk, int32_t hv, int32_t dk,
+                               int32_t dv, int32_t chunk, gdn_dtype dtype,
+                               hipStream_t stream);
+
+/*
  * One decode step for a batch of B sequences, one token each (paper, Section
  * 3.2: the one-pass form with the gate-scaled state; Section 5.4 for decode
  * as a bandwidth/launch-shape problem). The state is read once and written

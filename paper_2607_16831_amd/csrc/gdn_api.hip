@@ -4,6 +4,8 @@
 // enqueues nothing and the checks can be exercised without a GPU.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "../../include/gdn.h"
 #include "gdn_launch.h"
 
@@ -109,6 +111,31 @@ size_t required_workspace(int32_t n_seqs, int64_t n_tokens, int32_t hqk, int32_t
       .total;
 }
 
+// Scratch of gdn_prefill_scratch: the prefill workspace of every call on a
+// device, held by the code object for as long as the process runs. In host
+// code `scratch` names a host-side stand-in, not device memory: every use
+// goes through the device address hipGetSymbolAddress returns, fetched once
+// per device with that device current.
+static __device__ __align__(256) unsigned char scratch[GDN_PREFILL_SCRATCH_MAX_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of `scratch` on the current device (nullptr on failure).
+void *scratch_address() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+      return nullptr;
+    addr[dev] = p;
+  }
+  return addr[dev];
+}
+
 // The gate inputs: either g and beta, or all four raw inputs of the gated
 // entry points.
 bool gate_present(const float *g, const float *beta, const gdn::GateArgs &gate) {
@@ -122,7 +149,8 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
                         const int32_t *cu_seqlens, const float *initial_state, void *o,
                         float *final_state, int32_t n_seqs, int64_t n_tokens, int32_t hqk,
                         int32_t hv, int32_t dk, int32_t dv, int32_t chunk, gdn_dtype dtype,
-                        void *workspace, size_t workspace_bytes, hipStream_t stream) {
+                        void *workspace, size_t workspace_bytes, hipStream_t stream,
+                        bool use_scratch = false) {
   if (n_seqs < 0 || n_tokens < 0 || n_tokens > INT32_MAX) return GDN_ERR_INVALID_ARG;
   if (check_heads(hqk, hv) != GDN_OK) return GDN_ERR_INVALID_ARG;
   if (dk <= 0 || dv <= 0) return GDN_ERR_INVALID_ARG;
@@ -143,6 +171,15 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
   if (n_tokens > 0 && (!q || !k || !v || !o || !gate_present(g, beta, gate)))
     return GDN_ERR_INVALID_ARG;
   const int seg_chunks = chunk == 1 ? 0 : gdn::chain_segment_chunks(n_tokens, hv, chunk, ca.seg);
+  if (use_scratch) {
+    // Size first (no HIP call for a refused size), then the device's array.
+    if (required_workspace(n_seqs, n_tokens, hqk, hv, dk, chunk, ca) >
+        (size_t)GDN_PREFILL_SCRATCH_MAX_BYTES)
+      return GDN_ERR_WORKSPACE;
+    workspace = scratch_address();
+    if (workspace == nullptr) return GDN_ERR_HIP;
+    workspace_bytes = (size_t)GDN_PREFILL_SCRATCH_MAX_BYTES;
+  }
   if (!workspace ||
       workspace_bytes < required_workspace(n_seqs, n_tokens, hqk, hv, dk, chunk, ca) ||
       (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
@@ -255,6 +292,18 @@ gdn_status gdn_prefill(const void *q, const void *k, const void *v,
   return prefill_impl(q, k, v, g, beta, gdn::GateArgs(), cu_seqlens, initial_state, o,
                       final_state, n_seqs, n_tokens, hqk, hv, dk, dv, chunk, dtype, workspace,
                       workspace_bytes, stream);
+}
+
+gdn_status gdn_prefill_scratch(const void *q, const void *k, const void *v,
+                               const float *g, const float *beta,
+                               const int32_t *cu_seqlens, const float *initial_state,
+                               void *o, float *final_state, int32_t n_seqs,
+                               int64_t n_tokens, int32_t hqk, int32_t hv, int32_t dk,
+                               int32_t dv, int32_t chunk, gdn_dtype dtype,
+                               hipStream_t stream) {
+  return prefill_impl(q, k, v, g, beta, gdn::GateArgs(), cu_seqlens, initial_state, o,
+                      final_state, n_seqs, n_tokens, hqk, hv, dk, dv, chunk, dtype, nullptr, 0,
+                      stream, true);
 }
 
 gdn_status gdn_prefill_gated(const void *q, const void *k, const void *v,

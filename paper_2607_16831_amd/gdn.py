@@ -21,7 +21,11 @@ GDN_BF16, GDN_F32 = 0, 1
 
 EXPORTS = ("gdn_status_string", "gdn_version", "gdn_prefill_workspace_size",
            "gdn_prefill_auto_chunk", "gdn_prefill", "gdn_decode", "gdn_prefill_gated",
-           "gdn_decode_gated")
+           "gdn_decode_gated", "gdn_prefill_scratch")
+
+# Size of the library's fixed prefill workspace on each device
+# (GDN_PREFILL_SCRATCH_MAX_BYTES in gdn.h).
+PREFILL_SCRATCH_MAX_BYTES = 128 << 20
 
 # Prefill chunk sizes: AUTO lets the library choose from the batch shape,
 # SERIAL runs the token-serial path; 16, 32 and 64 run the chunked path.
@@ -83,6 +87,9 @@ def lib() -> ctypes.CDLL:
         L.gdn_decode_gated.argtypes = [vp, vp, vp, fp, fp, fp, fp, fp, vp, i32, i32, i32,
                                        i32, i32, ctypes.c_int, vp]
         L.gdn_decode_gated.restype = ctypes.c_int
+        L.gdn_prefill_scratch.argtypes = [vp, vp, vp, fp, fp, ip, fp, vp, fp, i32, i64,
+                                          i32, i32, i32, i32, i32, ctypes.c_int, vp]
+        L.gdn_prefill_scratch.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -175,6 +182,14 @@ def prefill_raw(q, k, v, g, beta, cu_seqlens, initial_state, o, final_state,
                                  chunk, dtype, workspace, workspace_bytes, stream))
 
 
+def prefill_scratch_raw(q, k, v, g, beta, cu_seqlens, initial_state, o, final_state,
+                        n_seqs, n_tokens, hqk, hv, dk, dv, chunk, dtype, stream) -> int:
+    """Direct call of gdn_prefill_scratch with integer pointers; returns the status."""
+    return int(lib().gdn_prefill_scratch(q, k, v, g, beta, cu_seqlens, initial_state, o,
+                                         final_state, n_seqs, n_tokens, hqk, hv, dk, dv,
+                                         chunk, dtype, stream))
+
+
 def decode_raw(q, k, v, g, beta, state, o, batch, hqk, hv, dk, dv, dtype,
                stream) -> int:
     """Direct call of gdn_decode with integer pointers; returns the status."""
@@ -244,6 +259,42 @@ def prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor,
                      workspace.numel(), _stream(stream))
     if st != GDN_OK:
         raise GdnError("gdn_prefill", st)
+    return o, final_state
+
+
+def prefill_scratch(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor,
+                    beta: torch.Tensor, cu_seqlens: torch.Tensor,
+                    initial_state: Optional[torch.Tensor] = None, chunk: int = 64,
+                    o: Optional[torch.Tensor] = None,
+                    final_state: Optional[torch.Tensor] = None,
+                    stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """prefill() on the library's fixed per-device workspace (gdn_prefill_scratch):
+    no workspace argument, and nothing allocated when o and final_state are
+    given. Sizes whose workspace exceeds PREFILL_SCRATCH_MAX_BYTES raise
+    GdnError (GDN_ERR_WORKSPACE)."""
+    _check_cu(cu_seqlens)
+    N = cu_seqlens.shape[0] - 1
+    _check_shapes(q, k, v, q.shape[0] if q.dim() == 3 else -1, N,
+                  (("g", g), ("beta", beta)),
+                  (("initial_state", initial_state), ("final_state", final_state)), o)
+    T, hqk, dk = q.shape
+    hv, dv = v.shape[1], v.shape[2]
+    if o is None:
+        o = torch.empty((T, hv, dv), dtype=q.dtype, device=q.device)
+    if final_state is None:
+        final_state = torch.empty((N, hv, dv, dk), dtype=torch.float32, device=q.device)
+    _check_dev(q, k, v, g, beta, cu_seqlens, initial_state, o, final_state)
+    if cu_seqlens.dtype != torch.int32:
+        raise TypeError("cu_seqlens must be int32")
+    if g.dtype != torch.float32 or beta.dtype != torch.float32:
+        raise TypeError("g and beta must be float32")
+    if k.dtype != q.dtype or v.dtype != q.dtype or o.dtype != q.dtype:
+        raise TypeError("q, k, v and o must share one dtype")
+    st = prefill_scratch_raw(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(cu_seqlens),
+                             _ptr(initial_state), _ptr(o), _ptr(final_state), N, T, hqk, hv,
+                             dk, dv, chunk, _dtype_code(q), _stream(stream))
+    if st != GDN_OK:
+        raise GdnError("gdn_prefill_scratch", st)
     return o, final_state
 
 

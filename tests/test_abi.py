@@ -301,3 +301,36 @@ def test_binding_checks_every_shape_before_launch():
                           final_state=torch.zeros(N + 1, hv, d, d))
     with pytest.raises(ValueError, match="^state must have shape"):
         gdn.decode_gated(dq, dq, dv, dg, dg, hvec, hvec, torch.zeros(B, hv, d, 2 * d))
+
+
+def test_scratch_prefill_validation():
+    """gdn_prefill_scratch refuses, before any HIP call, what gdn_prefill
+    refuses, and sizes whose workspace exceeds the library's fixed array."""
+    E = gdn
+
+    def call(**kw):
+        args = dict(q=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE, cu_seqlens=FAKE,
+                    initial_state=None, o=FAKE, final_state=FAKE, n_seqs=1, n_tokens=64,
+                    hqk=1, hv=1, dk=32, dv=32, chunk=16, dtype=gdn.GDN_F32, stream=None)
+        args.update(kw)
+        return gdn.prefill_scratch_raw(**args)
+
+    assert call(n_seqs=-1) == E.GDN_ERR_INVALID_ARG
+    assert call(hqk=2, hv=3) == E.GDN_ERR_INVALID_ARG
+    assert call(dk=96, dv=96) == E.GDN_ERR_UNSUPPORTED
+    assert call(chunk=48) == E.GDN_ERR_UNSUPPORTED
+    assert call(q=None) == E.GDN_ERR_INVALID_ARG
+    assert call(final_state=None) == E.GDN_ERR_INVALID_ARG
+    assert call(n_seqs=0, n_tokens=0, q=None, cu_seqlens=None) == E.GDN_OK
+    # 8192 tokens at 16/32 heads, d = 128, chunk 64: 131 MiB > 128 MiB
+    big = dict(n_tokens=8192, hqk=16, hv=32, dk=128, dv=128, chunk=64, dtype=gdn.GDN_BF16)
+    assert gdn.prefill_workspace_size(1, 8192, 16, 32, 128, 128, 64) > \
+        gdn.PREFILL_SCRATCH_MAX_BYTES
+    assert call(**big) == E.GDN_ERR_WORKSPACE
+    assert call(**dict(big, chunk=0)) == E.GDN_ERR_WORKSPACE
+    assert gdn.prefill_workspace_size(1, 4096, 16, 32, 128, 128, 64) <= \
+        gdn.PREFILL_SCRATCH_MAX_BYTES
+    # the header and the binding agree on the array's size
+    text = open(HEADER).read()
+    assert "#define GDN_PREFILL_SCRATCH_MAX_BYTES (128u << 20)" in text
+    assert gdn.PREFILL_SCRATCH_MAX_BYTES == 128 << 20
