@@ -65,7 +65,7 @@ typedef enum gdn_status {
 
 typedef enum gdn_dtype {
   GDN_BF16 = 0, /* q, k, v, o are bfloat16; o is rounded to nearest even */
-  GDN_F32 = 1   /* q, k, v, o are float32                                 */
+  GDN_F32 = 1   /* q, k, v, o are float32; computed in float32 throughout  */
 } gdn_dtype;
 
 /*
@@ -157,7 +157,10 @@ int32_t gdn_prefill_auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hqk,
  * Precision of the chunked path: bf16 inputs enter the matrix products as
  * bf16 operands with float32 accumulation, and the state is carried in
  * float32 (rel-L2 against an fp64 evaluation of the recurrence about 2e-3
- * to 4e-3 on o and the final state at the benchmark sizes).
+ * to 4e-3 on o and the final state at the benchmark sizes). float32 inputs
+ * are computed in float32 throughout, products and tables included (rel-L2
+ * about 1e-7 to 1e-6); for them GDN_CHUNK_NEUMANN changes nothing, the
+ * carry forms above do not apply, and the workspace goes unused.
  *
  * chunk = 1 runs the token-serial form instead: the recurrence token by
  * token in float32 on the vector ALU, the state held in registers for the
@@ -195,9 +198,9 @@ gdn_status gdn_prefill(const void *q, const void *k, const void *v,
  *
  * Sizes whose workspace (gdn_prefill_workspace_size with the same `chunk`)
  * exceeds GDN_PREFILL_SCRATCH_MAX_BYTES are refused with GDN_ERR_WORKSPACE
- * before any HIP call; the 128 MiB hold, for example, one 4096-token
- * sequence with 16 query/key and 32 value heads of size 128 at chunk 64
- * (66 MiB). Every call on one device shares that device's array: calls that
+ * before any HIP call; the 128 MiB hold, for example, one sequence of up
+ * to 10240 tokens with 16 query/key and 32 value heads of size 128 at
+ * chunk 64 (4096 tokens: 50 MiB). Every call on one device shares that device's array: calls that
  * overlap in time on one device (different streams, or different host
  * threads without ordering) race and give undefined results; calls ordered
  * on one stream do not. GDN_ERR_HIP if the array's address cannot be

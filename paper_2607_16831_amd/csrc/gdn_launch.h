@@ -52,7 +52,6 @@ struct PrefillWorkspace {
   size_t tfrag;       // bf16 [chunks, HV, FRAG]: (I + A)^-1 in operand order
   size_t pfrag;       // bf16 [chunks, HV, FRAG]: decay-masked Q K^T, same order
   size_t qfrag;       // bf16 [chunks, HQK, C * D]: Q in operand order (per-tile carry)
-  size_t kcopy;       // bf16 [chunks, HQK, C, D]: K rounded to bf16 (f32 inputs)
   // Segment maps of the whole-chain carry (n_maps slots; none when no
   // sequence can span more than one segment):
   size_t bslot;       // f32  [n_maps, HV, D, D]: B of a segment, then the composed state
@@ -95,14 +94,18 @@ PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
                                           int hv, int d, int chunk, int seg_chunks, bool tile);
 
 hipError_t launch_decode(const DecodeArgs &a);
-// Chunked prefill (chunk 16, 32 or 64) and the token-serial prefill (chunk 1,
-// no workspace).
+// Chunked prefill (chunk 16, 32 or 64; bf16 inputs through the chunk-local
+// kernel and a carry, float32 inputs through launch_prefill_f32) and the
+// token-serial prefill (chunk 1, no workspace).
 hipError_t launch_prefill(const PrefillArgs &a, const PrefillWorkspace &ws);
 // The whole-chain carry and the per-tile carry (bf16 inputs), after the
 // chunk-local kernel.
 hipError_t launch_chain_d(const PrefillArgs &a, const PrefillWorkspace &ws);
 hipError_t launch_tile_carry(const PrefillArgs &a, const PrefillWorkspace &ws);
 hipError_t launch_prefill_serial(const PrefillArgs &a);
+// float32 inputs, chunk 16, 32 or 64: float32 matrix products and tables
+// throughout (no workspace).
+hipError_t launch_prefill_f32(const PrefillArgs &a);
 
 // Compute units of the current device, read once per process.
 int device_compute_units();

@@ -124,8 +124,8 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     const float *__restrict__ g, const float *__restrict__ beta, GateArgs gate,
     const int32_t *__restrict__ cu, int n_seqs, int hqk, int hv, int group,
     int n_pairs, float *__restrict__ dec_ws, uint16_t *__restrict__ tfrag,
-    uint16_t *__restrict__ pfrag, uint16_t *__restrict__ qfrag,
-    uint16_t *__restrict__ kcopy) {
+    uint16_t *__restrict__ pfrag, uint16_t *__restrict__ qfrag) {
+  static_assert(sizeof(TIn) == 2, "bf16 inputs (float32 inputs take prefill_f32.hip)");
   using F = Cfg<D, C>;
   using LL = LocalLds<D, C>;
   constexpr int NIB = F::NIB, KS = F::KS, AP = LL::AP;
@@ -198,42 +198,20 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     gl = buf_load_f32(rg, (uint32_t)(lane * hv + h) * 4u);
     bta = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
   }
-  if constexpr (sizeof(TIn) == 2) {
-    // Buffer-to-LDS copies: lane i of a copy fills bytes [16 i, 16 i + 16) of
-    // its 1 KB piece, so the source offset picks the global 16-byte piece that
-    // belongs at that swizzled position.
+  // Buffer-to-LDS copies: lane i of a copy fills bytes [16 i, 16 i + 16) of
+  // its 1 KB piece, so the source offset picks the global 16-byte piece that
+  // belongs at that swizzled position.
 #pragma unroll
-    for (int it = 0; it < (2 * NKI + 3) / 4; ++it) {
-      const int m = wave + 4 * it;
-      if (m >= 2 * NKI) break;
-      const bool isq = m >= NKI;
-      const int mm = isq ? m - NKI : m;
-      const int u = 64 * mm + lane, row = u / KPR;
-      const int gp = (u % KPR) ^ kn_swizzle<D>(row);
-      const uint32_t off = (uint32_t)((row * hqk * D + 8 * gp) * 2);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(isq ? rq : rk, (lds_void *)((isq ? Qt : Kt) + 512 * mm),
-                                               16, off, 0, 0, 0);
-    }
-  } else {
-    constexpr int NP = C * KPR;
-    constexpr int NL = (NP + 255) / 256;
-    uint4 kv[NL], qv[NL];
-#pragma unroll
-    for (int u = 0; u < NL; ++u) {
-      const int idx = min(tid + 256 * u, NP - 1);
-      const uint32_t e = (uint32_t)((idx / KPR) * hqk * D + (idx % KPR) * 8);
-      kv[u] = BufElem<TIn>::load8(rk, e);
-      qv[u] = BufElem<TIn>::load8(rq, e);
-    }
-#pragma unroll
-    for (int u = 0; u < NL; ++u) {
-      const int idx = tid + 256 * u;
-      if (idx < NP) {
-        const int x = kn_index<D>(idx / KPR, 8 * (idx % KPR));
-        *reinterpret_cast<uint4 *>(&Kt[x]) = kv[u];
-        *reinterpret_cast<uint4 *>(&Qt[x]) = qv[u];
-      }
-    }
+  for (int it = 0; it < (2 * NKI + 3) / 4; ++it) {
+    const int m = wave + 4 * it;
+    if (m >= 2 * NKI) break;
+    const bool isq = m >= NKI;
+    const int mm = isq ? m - NKI : m;
+    const int u = 64 * mm + lane, row = u / KPR;
+    const int gp = (u % KPR) ^ kn_swizzle<D>(row);
+    const uint32_t off = (uint32_t)((row * hqk * D + 8 * gp) * 2);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(isq ? rq : rk, (lds_void *)((isq ? Qt : Kt) + 512 * mm),
+                                             16, off, 0, 0, 0);
   }
   // gamma: inclusive prefix sum of g over the chunk, lane t holding token t
   // (lanes past the end and past C hold g = 0: they repeat the last value).
@@ -249,24 +227,15 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
 
   // ---- for the per-tile carry (qfrag not null): Q of this chunk in the
   // A-operand order of Q S^T, block ib, step s, lane (l16, g4) holding
-  // Q[16 ib + l16][32 s + 8 g4 + (0..7)]. For f32 inputs: a bf16 copy of K,
-  // row-major [C][D], for the carry. One value head of the group writes them.
-  if (gi == 0 && wave < NIB) {
+  // Q[16 ib + l16][32 s + 8 g4 + (0..7)]. One value head of the group writes
+  // them.
+  if (gi == 0 && wave < NIB && qfrag != nullptr) {
     const int64_t base = ((int64_t)cidx * hqk + hk) * (C * D);
-    if (qfrag != nullptr) {
-      uint16_t *qf = qfrag + base + ((int64_t)wave * F::DS * 64 + lane) * 8;
+    uint16_t *qf = qfrag + base + ((int64_t)wave * F::DS * 64 + lane) * 8;
 #pragma unroll
-      for (int s = 0; s < F::DS; ++s)
-        *reinterpret_cast<uint4 *>(qf + s * 512) =
-            *reinterpret_cast<const uint4 *>(&Qt[kn_index<D>(16 * wave + l16, 32 * s + 8 * g4)]);
-    }
-    if (sizeof(TIn) == 4) {
-      uint16_t *kc = kcopy + base + (int64_t)(16 * wave + l16) * D;
-#pragma unroll
-      for (int s = 0; s < F::DS; ++s)
-        *reinterpret_cast<uint4 *>(kc + 32 * s + 8 * g4) =
-            *reinterpret_cast<const uint4 *>(&Kt[kn_index<D>(16 * wave + l16, 32 * s + 8 * g4)]);
-    }
+    for (int s = 0; s < F::DS; ++s)
+      *reinterpret_cast<uint4 *>(qf + s * 512) =
+          *reinterpret_cast<const uint4 *>(&Qt[kn_index<D>(16 * wave + l16, 32 * s + 8 * g4)]);
   }
 
   // ---- Gram tiles (ib, jb), jb <= ib, of this wavefront's product. Lane
@@ -458,8 +427,8 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k, const TIn *__restrict__ v,
     const int32_t *__restrict__ cu, const float *__restrict__ dec_ws,
     const uint16_t *__restrict__ tfrag, const uint16_t *__restrict__ pfrag,
-    const uint16_t *__restrict__ kcopy, const float *s0, float *sT, TIn *__restrict__ o,
-    int n_units, int hqk, int hv, int group) {
+    const float *s0, float *sT, TIn *__restrict__ o, int n_units, int hqk, int hv, int group) {
+  static_assert(sizeof(TIn) == 2, "bf16 inputs (float32 inputs take prefill_f32.hip)");
   using F = Cfg<D, C>;
   using WC = WaveCfg<D, C>;
   constexpr int NIB = F::NIB, KS = F::KS, DS = F::DS, NKT = F::NKT, NVT = F::NVT;
@@ -499,18 +468,15 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
     }
   }
 
-  // bf16 K comes straight from the input, f32 K from its bf16 copy
-  const bool kcopied = sizeof(TIn) != 2;
-  const uint16_t *ksrc = kcopied ? kcopy : reinterpret_cast<const uint16_t *>(k);
-  const int kstride = kcopied ? D : hqk * D;
+  const uint16_t *ksrc = reinterpret_cast<const uint16_t *>(k);
+  const int kstride = hqk * D;
 
   for (int lc = 0; lc < nch; ++lc) {
     const int64_t t0 = seq_t0 + (int64_t)lc * C;
     const int nv = (int)min((int64_t)C, seq_t1 - t0);
     const int64_t slot = (c0 + lc) * hv + h;
     // ---- loads: K chunk into LDS (rows past nv read as zero), the tables
-    const rsrc_t rk = kcopied ? make_rsrc(ksrc + ((c0 + lc) * hqk + hk) * (C * D), C * D * 2)
-                              : make_rsrc(ksrc + (t0 * hqk + hk) * D, (uint32_t)(nv * hqk * D * 2));
+    const rsrc_t rk = make_rsrc(ksrc + (t0 * hqk + hk) * D, (uint32_t)(nv * hqk * D * 2));
 #pragma unroll
     for (int m = 0; m < WC::NKI; ++m) {
       // (the offset goes in as a plain scalar: with an array element as the
@@ -681,8 +647,6 @@ PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
   const bool wave = uses_wave_carry(n_seqs, n_tokens, chunk);
   w.qfrag = p;
   if (tile && !wave) p = align256(p + sizeof(uint16_t) * (size_t)nc * hqk * chunk * d);
-  w.kcopy = p;
-  p = align256(p + sizeof(uint16_t) * (size_t)nc * hqk * chunk * d);
   // Maps of every segment but the last of each sequence (whole-chain carry):
   // at most T / span slots, and none when every sequence fits in one segment.
   const int64_t span = (int64_t)chunk * seg_chunks;
@@ -705,9 +669,8 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
   float *dec = reinterpret_cast<float *>(base + ws.decay);
   uint16_t *tf = reinterpret_cast<uint16_t *>(base + ws.tfrag);
   uint16_t *pf = reinterpret_cast<uint16_t *>(base + ws.pfrag);
-  uint16_t *kc = reinterpret_cast<uint16_t *>(base + ws.kcopy);
-  uint16_t *qf = (sizeof(TIn) == 2 && a.tile_carry && !a.wave_carry)
-                     ? reinterpret_cast<uint16_t *>(base + ws.qfrag) : nullptr;
+  uint16_t *qf =
+      (a.tile_carry && !a.wave_carry) ? reinterpret_cast<uint16_t *>(base + ws.qfrag) : nullptr;
   const int group = a.hv / a.hqk;
 
   const int64_t nc = chunk_bound(a.n_seqs, a.n_tokens, C);
@@ -719,23 +682,22 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
                            : chunk_local_kernel<D, C, TIn, false>;
     hipLaunchKernelGGL(local, dim3((unsigned)lblocks), dim3(256), 0, a.stream, (const TIn *)a.q,
                        (const TIn *)a.k, a.g, a.beta, a.gate, a.cu_seqlens, a.n_seqs, a.hqk, a.hv,
-                       group, (int)pairs, dec, tf, pf, qf, kc);
+                       group, (int)pairs, dec, tf, pf, qf);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
 
-  // bf16 inputs: the per-tile carry for few chains, else the whole-chain
-  // carry, unless the average sequence fits in one chunk. f32 inputs (and
-  // short sequences): the single-wave carry, which walks sequences of any
-  // length.
-  if (sizeof(TIn) == 2 && !a.wave_carry)
+  // The per-tile carry for few chains, else the whole-chain carry, unless
+  // the average sequence fits in one chunk: then the single-wave carry, which
+  // walks sequences of any length.
+  if (!a.wave_carry)
     return a.tile_carry ? launch_tile_carry(a, ws) : launch_chain_d(a, ws);
   const int n_groups = a.n_seqs * a.hqk;
   const int wpu = (group * F::NVT + WaveCfg<D, C>::WAVES - 1) / WaveCfg<D, C>::WAVES;
   const int64_t wblocks = (int64_t)8 * ((n_groups + 7) / 8) * wpu;
   hipLaunchKernelGGL((chunk_wave_kernel<D, C, TIn>), dim3((unsigned)wblocks), dim3(256), 0,
                      a.stream, (const TIn *)a.q, (const TIn *)a.k, (const TIn *)a.v,
-                     a.cu_seqlens, dec, tf, pf, kc, a.initial_state, a.final_state, (TIn *)a.o,
+                     a.cu_seqlens, dec, tf, pf, a.initial_state, a.final_state, (TIn *)a.o,
                      n_groups, a.hqk, a.hv, group);
   return hipGetLastError();
 }
@@ -761,8 +723,8 @@ static hipError_t launch_prefill_e(const PrefillArgs &a, const PrefillWorkspace 
 }
 
 hipError_t launch_prefill(const PrefillArgs &a, const PrefillWorkspace &ws) {
-  return a.dtype == GDN_BF16 ? launch_prefill_e<__bf16>(a, ws)
-                             : launch_prefill_e<float>(a, ws);
+  // float32 inputs: the float32-throughout form (prefill_f32.hip), no workspace
+  return a.dtype == GDN_BF16 ? launch_prefill_e<__bf16>(a, ws) : launch_prefill_f32(a);
 }
 
 }  // namespace gdn

@@ -136,7 +136,7 @@ constexpr int loader_copies() {
 template <int D, int C, typename TIn, int LW>
 __device__ __forceinline__ void carry_loader(
     CarryLds<D, C, TIn> &L, int lane, const uint16_t *__restrict__ ksrc, int kstride,
-    bool kcopied, const TIn *__restrict__ v, const float *__restrict__ dec_ws, int nch,
+    const TIn *__restrict__ v, const float *__restrict__ dec_ws, int nch,
     int64_t seq_t0, int64_t seq_t1, int64_t c0, int h, int hk, int hqk, int hv, int v0) {
   using CC = CarryCfg<D, C, TIn>;
   constexpr int NS = CC::SLOTS;
@@ -148,10 +148,7 @@ __device__ __forceinline__ void carry_loader(
     const int64_t t0 = seq_t0 + (int64_t)lc * C;
     const int nv = (int)min((int64_t)C, seq_t1 - t0);
     CopyRes r;
-    if (kcopied)  // bf16 copy in the workspace, [chunk slot][key head][C][D]
-      r.k = make_rsrc(ksrc + ((c0 + lc) * hqk + hk) * (C * D), C * D * 2);
-    else
-      r.k = make_rsrc(ksrc + (t0 * hqk + hk) * D, (uint32_t)(nv * hqk * D * 2));
+    r.k = make_rsrc(ksrc + (t0 * hqk + hk) * D, (uint32_t)(nv * hqk * D * 2));
     r.v = make_rsrc(v + (t0 * hv + h) * D + v0, (uint32_t)(nv * hv * D * CC::ESZ));
     r.d = make_rsrc(dec_ws + ((c0 + lc) * hv + h) * 2 * C, 2 * C * 4);
     return r;
@@ -432,8 +429,7 @@ __global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
     const TIn *__restrict__ k, const TIn *__restrict__ v,
     const int32_t *__restrict__ cu, const float *__restrict__ dec_ws,
     const uint16_t *__restrict__ tfrag, const uint16_t *__restrict__ pfrag,
-    const uint16_t *__restrict__ qfrag, const uint16_t *__restrict__ kcopy,
-    const float *s0, float *sT, TIn *__restrict__ o, int hqk, int hv, int group,
+    const uint16_t *__restrict__ qfrag, const float *s0, float *sT, TIn *__restrict__ o, int hqk, int hv, int group,
     int n_groups) {
   using F = Cfg<D, C>;
   using CC = CarryCfg<D, C, TIn>;
@@ -493,17 +489,15 @@ __global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
         carry_compute_o<D, C, TIn>(L, S, wave, lane, nch, c0, pfrag, qfrag, o, seq_t0, seq_t1,
                                    h, hk, hqk, hv, v0);
     } else {
-      // bf16 K is copied straight from the input; f32 K from its bf16 copy.
-      const bool kcopied = sizeof(TIn) != 2;
-      const uint16_t *ksrc = kcopied ? kcopy : reinterpret_cast<const uint16_t *>(k);
-      const int kstride = kcopied ? D : hqk * D;
+      const uint16_t *ksrc = reinterpret_cast<const uint16_t *>(k);
+      const int kstride = hqk * D;
       static_assert(CC::NLW == 2, "loader dispatch below");
       if (wave == CC::NCW)
-        carry_loader<D, C, TIn, 0>(L, lane, ksrc, kstride, kcopied, v, dec_ws, nch, seq_t0,
-                                   seq_t1, c0, h, hk, hqk, hv, v0);
+        carry_loader<D, C, TIn, 0>(L, lane, ksrc, kstride, v, dec_ws, nch, seq_t0, seq_t1, c0,
+                                   h, hk, hqk, hv, v0);
       else
-        carry_loader<D, C, TIn, 1>(L, lane, ksrc, kstride, kcopied, v, dec_ws, nch, seq_t0,
-                                   seq_t1, c0, h, hk, hqk, hv, v0);
+        carry_loader<D, C, TIn, 1>(L, lane, ksrc, kstride, v, dec_ws, nch, seq_t0, seq_t1, c0,
+                                   h, hk, hqk, hv, v0);
     }
   }
 
@@ -520,13 +514,12 @@ static hipError_t launch_tile_carry_t(const PrefillArgs &a, const PrefillWorkspa
   const uint16_t *tf = reinterpret_cast<const uint16_t *>(base + ws.tfrag);
   const uint16_t *pf = reinterpret_cast<const uint16_t *>(base + ws.pfrag);
   const uint16_t *qf = reinterpret_cast<const uint16_t *>(base + ws.qfrag);
-  const uint16_t *kc = reinterpret_cast<const uint16_t *>(base + ws.kcopy);
   const int group = a.hv / a.hqk;
   const int n_groups = a.n_seqs * a.hqk;
   const int64_t blocks = (int64_t)8 * ((n_groups + 7) / 8) * group * F::NVT;
   hipLaunchKernelGGL((chunk_carry_kernel<D, C, TIn>), dim3((unsigned)blocks),
                      dim3(kCarryThreads), 0, a.stream, (const TIn *)a.k, (const TIn *)a.v,
-                     a.cu_seqlens, dec, tf, pf, qf, kc, a.initial_state, a.final_state,
+                     a.cu_seqlens, dec, tf, pf, qf, a.initial_state, a.final_state,
                      (TIn *)a.o, a.hqk, a.hv, group, n_groups);
   return hipGetLastError();
 }

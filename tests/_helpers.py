@@ -5,6 +5,14 @@ import torch
 # Parity bars (rel-L2 against the fp64 oracle): bf16 outputs and fp32 state.
 O_BAR = 2e-2
 STATE_BAR = 5e-3
+# float32 inputs on the chunked path: float32 products and tables throughout,
+# held to the canary bar on o and on the state.
+F32_BAR = 1e-4
+
+
+def chunked_bars(dtype):
+    """(o bar, state bar) of the chunked path for an input dtype."""
+    return (O_BAR, STATE_BAR) if dtype == "bf16" else (F32_BAR, F32_BAR)
 
 
 def rel_l2(x, y) -> float:

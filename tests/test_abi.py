@@ -322,9 +322,9 @@ def test_scratch_prefill_validation():
     assert call(q=None) == E.GDN_ERR_INVALID_ARG
     assert call(final_state=None) == E.GDN_ERR_INVALID_ARG
     assert call(n_seqs=0, n_tokens=0, q=None, cu_seqlens=None) == E.GDN_OK
-    # 8192 tokens at 16/32 heads, d = 128, chunk 64: 131 MiB > 128 MiB
-    big = dict(n_tokens=8192, hqk=16, hv=32, dk=128, dv=128, chunk=64, dtype=gdn.GDN_BF16)
-    assert gdn.prefill_workspace_size(1, 8192, 16, 32, 128, 128, 64) > \
+    # 16384 tokens at 16/32 heads, d = 128, chunk 64: 197 MiB > 128 MiB
+    big = dict(n_tokens=16384, hqk=16, hv=32, dk=128, dv=128, chunk=64, dtype=gdn.GDN_BF16)
+    assert gdn.prefill_workspace_size(1, 16384, 16, 32, 128, 128, 64) > \
         gdn.PREFILL_SCRATCH_MAX_BYTES
     assert call(**big) == E.GDN_ERR_WORKSPACE
     assert call(**dict(big, chunk=0)) == E.GDN_ERR_WORKSPACE

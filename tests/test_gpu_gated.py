@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import oracle
-from _helpers import O_BAR, STATE_BAR, gates_from_raw, rel_l2, require_gpu, to_dev
+from _helpers import O_BAR, chunked_bars, gates_from_raw, rel_l2, require_gpu, to_dev
 from paper_2607_16831_amd import gdn, synth
 
 pytestmark = pytest.mark.gpu
@@ -44,7 +44,8 @@ def test_prefill_gated_vs_oracle(dtype, d, chunk):
     eo, es = rel_l2(o.cpu(), o_ref), rel_l2(sT.cpu(), s_ref)
     _log("prefill_gated_%s_d%d_C%d" % (dtype, d, chunk), o=eo, state=es)
     assert torch.isfinite(o.float()).all() and torch.isfinite(sT).all()
-    assert eo <= O_BAR and es <= STATE_BAR
+    ob, sb = chunked_bars(dtype)
+    assert eo <= ob and es <= sb
 
 
 def test_prefill_gated_matches_plain():

@@ -19,7 +19,7 @@ import pytest
 import torch
 
 import oracle
-from _helpers import O_BAR, STATE_BAR, chain_errors, rel_l2, require_gpu, to_dev
+from _helpers import O_BAR, STATE_BAR, F32_BAR, chain_errors, chunked_bars, rel_l2, require_gpu, to_dev
 from paper_2607_16831_amd import gdn, synth
 
 pytestmark = pytest.mark.gpu
@@ -142,7 +142,9 @@ def test_decode_repeated_steps_match_prefill():
 # ------------------------------------------------------------------ prefill
 def test_prefill_tiny_f32():
     dev = require_gpu()
-    check_full("prefill_tiny", synth.make(synth.PREFILL_TINY), dev)
+    # float32 throughout: the canary bar on o and the state
+    check_full("prefill_tiny", synth.make(synth.PREFILL_TINY), dev, o_bar=F32_BAR,
+               s_bar=F32_BAR)
 
 
 def test_prefill_4k_full():
@@ -213,7 +215,9 @@ def test_prefill_shapes(d, chunk, dtype):
     w = synth.PREFILL_4K.replace(seq_len=None, lengths=(37, 0, 100, 16, 64),
                                  n_seqs=5, hqk=2, hv=4, d=d, dtype=dtype,
                                  g_mu=-2.0, state_std=0.1, seed=41)
-    check_full("shape_d%d_C%d_%s" % (d, chunk, dtype), synth.make(w), dev, chunk=chunk)
+    ob, sb = chunked_bars(dtype)
+    check_full("shape_d%d_C%d_%s" % (d, chunk, dtype), synth.make(w), dev, chunk=chunk,
+               o_bar=ob, s_bar=sb)
 
 
 def test_prefill_alias_in_place():
@@ -232,8 +236,9 @@ def test_prefill_ragged_c16(alias, dtype):
     w = synth.PREFILL_4K.replace(seq_len=None, lengths=(150, 0, 33, 200, 5), n_seqs=5,
                                  hqk=2, hv=4, d=64, dtype=dtype, g_mu=-4.0,
                                  state_std=0.1, seed=53)
+    ob, sb = chunked_bars(dtype)
     check_full("ragged_c16_alias%d_%s" % (alias, dtype), synth.make(w), dev, chunk=16,
-               alias=alias)
+               alias=alias, o_bar=ob, s_bar=sb)
 
 
 def test_prefill_group4_and_group1():

@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import oracle
-from _helpers import O_BAR, STATE_BAR, chain_errors, rel_l2, require_gpu, to_dev
+from _helpers import chain_errors, chunked_bars, rel_l2, require_gpu, to_dev
 from paper_2607_16831_amd import gdn, synth
 
 pytestmark = pytest.mark.gpu
@@ -66,7 +66,7 @@ def test_random_configuration(seed):
     if serial:
         ob, sb = (4e-3 if dtype == "bf16" else 1e-5), 2e-5
     else:
-        ob, sb = O_BAR, STATE_BAR
+        ob, sb = chunked_bars(dtype)
     assert eo <= ob and es <= sb
     assert e["o_max"] <= ob and e["state_max"] <= sb
 

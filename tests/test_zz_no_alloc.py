@@ -2,7 +2,7 @@
 gdn_prefill on the GPU.
 
 Both run the same kernels, so the outputs must agree bit for bit. Two calls
-in a row: the 4096-token workload (16/32 heads, d = 128, chunk 64: a 66 MiB
+in a row: the 4096-token workload (16/32 heads, d = 128, chunk 64: a 50 MiB
 workspace), then a smaller ragged batch with initial states and another
 chunk size, which runs over whatever the first call left in the library's
 array. Both are also held to the oracle's bars.
@@ -53,8 +53,8 @@ def test_scratch_entry_matches_workspace_entry_twice():
 
 def test_scratch_entry_refuses_oversized_workspace():
     dev = require_gpu()
-    x = to_dev(synth.make(synth.PREFILL_4K.replace(seq_len=8192, hqk=16, hv=32)), dev)
-    assert gdn.prefill_workspace_size(1, 8192, 16, 32, 128, 128, 64) > \
+    x = to_dev(synth.make(synth.PREFILL_4K.replace(seq_len=16384, hqk=16, hv=32)), dev)
+    assert gdn.prefill_workspace_size(1, 16384, 16, 32, 128, 128, 64) > \
         gdn.PREFILL_SCRATCH_MAX_BYTES
     with pytest.raises(gdn.GdnError) as err:
         gdn.prefill_scratch(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu_seqlens"],
