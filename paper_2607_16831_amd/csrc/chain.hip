@@ -52,10 +52,13 @@ namespace gdn {
 template <int D, int C, bool MAPS>
 struct ChainCfg {
   using F = Cfg<D, C>;
-  // 16-row value tiles per compute wavefront: two at d = 128, so that every
-  // chunk operand read from LDS feeds two matrix products (LDS reads, not the
-  // matrix cores, bound the chunk step).
-  static constexpr int NJ = D == 128 ? 2 : 1;
+  // 16-row value tiles per compute wavefront. One in the output launch: its
+  // eight compute wavefronts put two on each SIMD, which hides the latency
+  // of the chunk step's dependent LDS reads and products better than four
+  // wavefronts of two tiles each (measured on the 66K-token batch of 16
+  // sequences: 1.20 -> 1.07 ms per call). Two in the map launch at d = 128,
+  // which carries twice the rows and would exceed the work-group size.
+  static constexpr int NJ = (D == 128 && MAPS) ? 2 : 1;
   static constexpr int NWR = D / (16 * NJ);     // compute wavefronts per set of D rows
   static constexpr int NCW = MAPS ? 2 * NWR : NWR;  // compute wavefronts
   static constexpr int NT = 64 * (NCW + 2);     // threads: compute, a loader and a prefetcher

@@ -71,12 +71,34 @@ struct CarryLds {
   uint16_t Kn[CC::NB][F::CP * D];  // K chunk, row-major, swizzled; rows C..CP-1 stay zero
   uint4 Vl[CC::NB][CC::NVI * 64];  // V tile, [token][16 values], input element type
   float Dl[CC::NB][CC::NDI * 256];  // exp(gamma_i), then exp(gamma_last - gamma_i)
-  uint16_t Sl[16 * F::LDK];     // bf16 copy of the state tile, [value][key]
-  uint16_t Yl[16 * F::LDV];     // Y,  [value][token position]
-  uint16_t Ul[16 * F::LDV];     // U,  [value][token position]
-  uint16_t Uh[16 * F::LDV];     // exp(gamma_last - gamma) U, same layout
+  // The tiles exchanged between wavefronts, stored in the B-operand order of
+  // the products that read them: contraction step s is 64 lanes x 16 bytes,
+  // contiguous, so each operand read is one conflict-free 1 KB block
+  // (row-major tiles with padded rows took two LDS passes per read).
+  uint16_t Sl[F::DS * 512];     // bf16 copy of the state tile (key order)
+  uint16_t Yl[F::KS * 512];     // Y (token order of tok_pos)
+  uint16_t Ul[F::KS * 512];     // U
+  uint16_t Uh[F::KS * 512];     // exp(gamma_last - gamma) U
 };
 
+
+// Element index, in a B-operand-ordered tile, of the 4 values a lane holds
+// in accumulator layout:
+//  - state tile `t` (keys 16 t + 4 g4 + [0, 4) of row l16): step t / 2,
+//    operand lane 16 (2 (t % 2) + g4 / 2) + l16, half g4 % 2. The 64 lanes of
+//    one key tile write 512 contiguous bytes (conflict-free 8-byte stores).
+//  - token block `ib` (tokens 16 ib + 4 g4 + [0, 4), row l16): step ib / 2,
+//    operand lane 16 g4 + l16, half ib % 2 (the token order of tok_pos).
+__device__ __forceinline__ int s_slot(int t, int l16, int g4) {
+  return ((t >> 1) * 64 + 16 * (2 * (t & 1) + (g4 >> 1)) + l16) * 8 + 4 * (g4 & 1);
+}
+__device__ __forceinline__ int y_slot(int ib, int l16, int g4) {
+  return ((ib >> 1) * 64 + 16 * g4 + l16) * 8 + 4 * (ib & 1);
+}
+// Operand of step s for lane `lane`.
+__device__ __forceinline__ uint4 op_read(const uint16_t *T, int s, int lane) {
+  return *reinterpret_cast<const uint4 *>(&T[(s * 64 + lane) * 8]);
+}
 
 // ---------------------------------------------------------------- loaders
 // Copy m of a chunk, in order: K, V tile, decay factors, each 16 bytes per
@@ -204,13 +226,13 @@ __device__ __forceinline__ void state_update(CarryLds<D, C, TIn> &L, f32x4 &S, c
   uint4 bu[F::KS];
 #pragma unroll
   for (int s = 0; s < F::KS; ++s)
-    bu[s] = *reinterpret_cast<const uint4 *>(&L.Uh[l16 * F::LDV + 32 * s + 8 * g4]);
+    bu[s] = op_read(L.Uh, s, 16 * g4 + l16);
   f32x4 acc = S * glast;
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int s = 0; s < F::KS; ++s) acc = mfma_16x16x32(kt[s], bu[s], acc);
   S = acc;
-  *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
+  *reinterpret_cast<uint2 *>(&L.Sl[s_slot(wave, l16, g4)]) =
       pack4_bf16(acc[0], acc[1], acc[2], acc[3]);
 }
 
@@ -232,7 +254,6 @@ __device__ __forceinline__ void carry_compute_xu(
   // never stored, and read through an offset past the resource (zeros).
   const int nks = min(ibc / 2 + 1, F::KS);
   const int tb = 16 * ibc + 4 * g4;                     // this lane's first token
-  const int ypos = 32 * (ib >> 1) + 8 * g4 + 4 * (ib & 1);  // tok_pos(16 ib + 4 g4)
   const uint32_t foff = (uint32_t)(((ibc * F::KS) * 64 + lane) * 16);
   auto frag_res = [&](int lc) {
     return make_rsrc(tfrag + ((c0 + lc) * hv + h) * F::FRAG, F::FRAG * 2);
@@ -275,12 +296,12 @@ __device__ __forceinline__ void carry_compute_xu(
       uint4 bs[F::DS];
 #pragma unroll
       for (int s = 0; s < F::DS; ++s)
-        bs[s] = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
+        bs[s] = op_read(L.Sl, s, lane);
       __builtin_amdgcn_sched_barrier(0);
       f32x4 xs = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < F::DS; ++s) xs = mfma_16x16x32(ka[s], bs[s], xs);
-      *reinterpret_cast<uint2 *>(&L.Yl[l16 * F::LDV + ypos]) =
+      *reinterpret_cast<uint2 *>(&L.Yl[y_slot(ib, l16, g4)]) =
           pack4_bf16(vv[0] - ge[0] * xs[0], vv[1] - ge[1] * xs[1], vv[2] - ge[2] * xs[2],
                      vv[3] - ge[3] * xs[3]);
     }
@@ -290,13 +311,13 @@ __device__ __forceinline__ void carry_compute_xu(
       uint4 by[F::KS];
 #pragma unroll
       for (int s = 0; s < F::KS; ++s)
-        by[s] = *reinterpret_cast<const uint4 *>(&L.Yl[l16 * F::LDV + 32 * s + 8 * g4]);
+        by[s] = op_read(L.Yl, s, lane);
       __builtin_amdgcn_sched_barrier(0);
       f32x4 u = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < F::KS; ++s) u = mfma_16x16x32(fa[s], by[s], u);
-      *reinterpret_cast<uint2 *>(&L.Ul[l16 * F::LDV + ypos]) = pack4_bf16(u[0], u[1], u[2], u[3]);
-      *reinterpret_cast<uint2 *>(&L.Uh[l16 * F::LDV + ypos]) =
+      *reinterpret_cast<uint2 *>(&L.Ul[y_slot(ib, l16, g4)]) = pack4_bf16(u[0], u[1], u[2], u[3]);
+      *reinterpret_cast<uint2 *>(&L.Uh[y_slot(ib, l16, g4)]) =
           pack4_bf16(he[0] * u[0], he[1] * u[1], he[2] * u[2], he[3] * u[3]);
       // reload after the last reader (the last chunk re-reads itself)
       __builtin_amdgcn_sched_barrier(0);
@@ -353,7 +374,7 @@ __device__ __forceinline__ void carry_compute_o(
     uint4 bu[F::KS];
 #pragma unroll
     for (int s = 0; s < F::KS; ++s)
-      bu[s] = *reinterpret_cast<const uint4 *>(&L.Ul[l16 * F::LDV + 32 * s + 8 * g4]);
+      bu[s] = op_read(L.Ul, s, 16 * g4 + l16);
     __builtin_amdgcn_sched_barrier(0);
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -402,7 +423,7 @@ __device__ __forceinline__ void carry_compute_o(
       uint4 bs[F::DS];
 #pragma unroll
       for (int s = 0; s < F::DS; ++s)
-        bs[s] = *reinterpret_cast<const uint4 *>(&L.Sl[l16 * F::LDK + 32 * s + 8 * g4]);
+        bs[s] = op_read(L.Sl, s, lane);
       __builtin_amdgcn_sched_barrier(0);
       f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -469,7 +490,7 @@ __global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
   if (nch > 0) {  // uniform over the work-group
     if (compute) {
       if (C < F::CP) {  // zero the token positions past the chunk, once
-        for (int idx = tid; idx < 16 * F::LDV; idx += 64 * CC::NCW) {
+        for (int idx = tid; idx < F::KS * 512; idx += 64 * CC::NCW) {
           L.Yl[idx] = 0;
           L.Ul[idx] = 0;
           L.Uh[idx] = 0;
@@ -480,7 +501,7 @@ __global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
         }
       }
       if (own)
-        *reinterpret_cast<uint2 *>(&L.Sl[l16 * F::LDK + 16 * wave + 4 * g4]) =
+        *reinterpret_cast<uint2 *>(&L.Sl[s_slot(wave, l16, g4)]) =
             pack4_bf16(S[0], S[1], S[2], S[3]);
       lds_barrier();
       if (wave < 4)
