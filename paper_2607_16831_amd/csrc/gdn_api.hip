@@ -94,10 +94,11 @@ ChunkArg parse_chunk(int32_t chunk) {
   return c;
 }
 
-// The carry of a chunked call: the per-tile carry when forced, or when no
-// segment length is forced and the batch has few chains.
-bool tile_carry(const ChunkArg &c, int32_t n_seqs, int32_t hv, int32_t d) {
-  return c.tiles || (c.seg == 0 && gdn::uses_tile_carry(n_seqs, hv, d));
+// The carry of a chunked call (chunk resolved): the per-tile carry when
+// forced, or when no segment length is forced and the whole-chain carry
+// would not fill the chip.
+bool tile_carry(const ChunkArg &c, int32_t n_seqs, int64_t n_tokens, int32_t hv, int32_t chunk) {
+  return c.tiles || (c.seg == 0 && gdn::uses_tile_carry(n_seqs, n_tokens, hv, chunk));
 }
 
 // Workspace bytes for a resolved chunk size. The token-serial path uses none;
@@ -107,7 +108,7 @@ size_t required_workspace(int32_t n_seqs, int64_t n_tokens, int32_t hqk, int32_t
   if (chunk == 1) return 256;
   const int L = gdn::chain_segment_chunks(n_tokens, hv, chunk, c.seg);
   return gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, d, chunk, L,
-                                       tile_carry(c, n_seqs, hv, d))
+                                       tile_carry(c, n_seqs, n_tokens, hv, chunk))
       .total;
 }
 
@@ -200,7 +201,7 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
   // work-group carry's fixed cost then outweighs its per-chunk speed.
   a.wave_carry = gdn::uses_wave_carry(n_seqs, n_tokens, chunk);
   a.seg_chunks = seg_chunks;
-  a.tile_carry = tile_carry(ca, n_seqs, hv, dk);
+  a.tile_carry = tile_carry(ca, n_seqs, n_tokens, hv, chunk);
   a.dtype = dtype;
   a.workspace = workspace;
   a.stream = stream;

@@ -72,13 +72,18 @@ inline int64_t chunk_bound(int n_seqs, int64_t n_tokens, int chunk) {
 // Chunks per segment of the whole-chain carry: `requested` if positive, else
 // enough that the segments of all chains give about kChainUnits work-groups.
 constexpr int kChainUnits = 256;
-// The whole-chain carry needs at least this many (sequence, value head)
-// chains, one work-group each, to fill the chip; with fewer the per-tile
-// carry spreads every chain over D/16 work-groups instead. Measured on the
-// 66K-token batch of 16 sequences (512 chains: whole-chain 1.20 ms, per-tile
-// 1.44 ms) and on 2 x 32768 tokens (64 chains: per-tile 1.47 ms, whole-chain
-// with segments 1.54 ms).
+// The whole-chain carry fills the chip when the batch has at least this many
+// (sequence, value head) chains, one work-group each, or when its automatic
+// segments are at least kChainMinSegment chunks long (long chains, cut into
+// enough segments, whose map and composition launches are then amortised).
+// Otherwise the per-tile carry spreads every chain over D/16 work-groups.
+// Measured (d = 128, 16/32 heads, C = 64): 66K tokens in 16 sequences (512
+// chains) whole-chain 1.07-1.10 ms, per-tile 1.43 ms; 2 x 32768 tokens (64
+// chains, segments of 128 chunks) 1.39 against 1.47 ms, with 64-chunk
+// segments 1.47 (even); 4096 tokens (32 chains, segments of 8 chunks) 139
+// against 82 us.
 constexpr int64_t kChainCarryMinChains = 256;
+constexpr int kChainMinSegment = 64;
 constexpr int kMinSegmentChunks = 4;
 int chain_segment_chunks(int64_t n_tokens, int hv, int chunk, int requested);
 // The whole-chain carry runs unless the average sequence fits in one chunk
@@ -86,10 +91,10 @@ int chain_segment_chunks(int64_t n_tokens, int hv, int chunk, int requested);
 inline bool uses_wave_carry(int n_seqs, int64_t n_tokens, int chunk) {
   return n_tokens <= (int64_t)n_seqs * chunk;
 }
-// The per-tile carry when the batch has fewer (sequence, value head) chains
-// than kChainCarryMinChains: every chain is then spread over D/16
-// work-groups without segments.
-bool uses_tile_carry(int n_seqs, int hv, int d);
+// The per-tile carry unless the whole-chain carry fills the chip (see
+// kChainCarryMinChains): every chain is then spread over D/16 work-groups
+// without segments.
+bool uses_tile_carry(int n_seqs, int64_t n_tokens, int hv, int chunk);
 PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
                                           int hv, int d, int chunk, int seg_chunks, bool tile);
 

@@ -629,8 +629,9 @@ int chain_segment_chunks(int64_t n_tokens, int hv, int chunk, int requested) {
   return (int)std::min<int64_t>(std::max<int64_t>(l, kMinSegmentChunks), 1 << 20);
 }
 
-bool uses_tile_carry(int n_seqs, int hv, int) {
-  return (int64_t)n_seqs * hv < kChainCarryMinChains;
+bool uses_tile_carry(int n_seqs, int64_t n_tokens, int hv, int chunk) {
+  return (int64_t)n_seqs * hv < kChainCarryMinChains &&
+         chain_segment_chunks(n_tokens, hv, chunk, 0) < kChainMinSegment;
 }
 
 PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,

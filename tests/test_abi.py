@@ -239,6 +239,11 @@ def test_carry_flags_sizes_and_validation():
     # many chains: the whole-chain carry (no Q fragments), segments picked by size
     big = ws(16, 66000, 16, 32, 128, 128, 64)
     assert big < ws(16, 66000, 16, 32, 128, 128, 64 | TILE)
+    # few but long chains (2 x 32768 tokens: 64 chains, automatic segments of
+    # 1024 * 32 / 256 = 128 chunks): the whole-chain carry as with S(128)
+    long = ws(2, 65536, 16, 32, 128, 128, 64)
+    assert long == ws(2, 65536, 16, 32, 128, 128, 64 | S(128))
+    assert long != ws(2, 65536, 16, 32, 128, 128, 64 | TILE)
     for bad in (1 | S(2), 1 | TILE, 64 | TILE | S(2), 64 | (1 << 30)):
         assert ws(1, 4096, 16, 32, 128, 128, bad) == 0
         assert _prefill(chunk=bad) == gdn.GDN_ERR_UNSUPPORTED
