@@ -45,8 +45,8 @@ METRIC = "prefill tokens/sec + MFMA util; decode µs/step + achieved HBM GB/s"
 # the kernel sources they were taken on. Any change to those sources makes
 # the figures stale, and `traffic` is then reported as null.
 MEASURED_TRAFFIC = {
-    "7d323696a095e55960df489773ededcaca48f0edfa7a4073447004182be4630e":
-        {"prefill": 233647352, "decode": 274399387},
+    "5b04a087d9e5ab5f06b1bf2b7b2e4f4b89549ba476c849f78c799911899c6ce4":
+        {"prefill": 224876278, "decode": 274400641},
 }
 
 
@@ -104,6 +104,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-decode-sweep", action="store_true",
                     help="skip the small-batch decode latency sweep")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="skip timing the 66K-token varlen batch and the 2 x 32768-token prefill")
     ap.add_argument("--no-dispatch-sweep", action="store_true",
                     help="skip the prefill shape-dispatch comparison over short-sequence batches")
     ap.add_argument("--segment", type=int, default=0, metavar="L",
@@ -331,6 +333,43 @@ def main():
             disp["N%d_L%d" % (N, L)] = row
             del t, o, fs, ws
         out["prefill_dispatch"] = disp
+
+    # ------------------------------------------------- larger prefill batches
+    # The varlen batch (16 sequences, lengths U[64, 8192], nonzero initial
+    # states) and the long-context pair (2 x 32768 tokens, strong decay), same
+    # heads and d: time per call (events, 5 calls after 2 warm-up calls, one
+    # input set each), with the algorithmic flop count of the same formula.
+    if not args.no_other_workloads:
+        other = {}
+        for w in (synth.PREFILL_VARLEN, synth.PREFILL_LONG):
+            y = synth.make(w)
+            t = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in y.items()}
+            Tw = t["q"].shape[0]
+            o = torch.empty((Tw, w.hv, w.d), dtype=torch.bfloat16, device=dev)
+            fs = torch.empty((w.n_seqs, w.hv, w.d, w.d), device=dev)
+            ws = gdn.alloc_workspace(w.n_seqs, Tw, w.hqk, w.hv, w.d, w.chunk, dev)
+
+            def call():
+                gdn.prefill(t["q"], t["k"], t["v"], t["g"], t["beta"], t["cu_seqlens"],
+                            initial_state=t["initial_state"], chunk=w.chunk, o=o,
+                            final_state=fs, workspace=ws)
+            for _ in range(2):
+                call()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(5):
+                call()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / 5
+            fl = prefill_flops(Tw, w.hqk, w.hv, w.d, w.chunk)
+            other[w.name] = {"tokens": Tw, "us_per_call": round(us, 1),
+                             "tokens_per_s": round(Tw / (us * 1e-6), 1),
+                             "tflops": round(fl / (us * 1e-6) / 1e12, 2),
+                             "mfma_util": round(fl / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+            del t, o, fs, ws
+        out["prefill_other_workloads"] = other
 
     # ---------------------------------------------------------------- oracle
     if not args.no_cpu_baseline:
