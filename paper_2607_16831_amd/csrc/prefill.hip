@@ -62,7 +62,7 @@ struct LocalLds {
   static constexpr int NBLK = NIB * (NIB + 1) / 2;  // lower blocks, diagonal included
   static constexpr int AP = 20;                     // f32 pitch of an A block row
   union {
-    uint16_t kq[2 * C * D];  // K tile, then Q tile; swizzled rows (kn_index)
+    uint16_t kq[C * D];  // K tile, swizzled rows (kn_index)
     struct {
       float A[NBLK][16 * AP];     // block (m, c) at m (m + 1) / 2 + c, row-major
       float linv[NIB][16 * 17];   // transposed diagonal inverses
@@ -133,7 +133,7 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
   constexpr int KPR = D / 8;        // 16-byte pieces per row
   static_assert(NIB == 1 || NIB == 2 || NIB == 4, "row sets");
   __shared__ __attribute__((aligned(16))) LL L;
-  uint16_t *Kt = L.u.kq, *Qt = L.u.kq + C * D;
+  uint16_t *Kt = L.u.kq;
 
   // Block id -> (chunk, key head) pair and head of the group. Work-groups are
   // dealt to the eight XCDs round robin, so ids b and b + 8 share one: the
@@ -198,20 +198,38 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     gl = buf_load_f32(rg, (uint32_t)(lane * hv + h) * 4u);
     bta = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
   }
-  // Buffer-to-LDS copies: lane i of a copy fills bytes [16 i, 16 i + 16) of
-  // its 1 KB piece, so the source offset picks the global 16-byte piece that
-  // belongs at that swizzled position.
+  // K: buffer-to-LDS copies (lane i of a copy fills bytes [16 i, 16 i + 16)
+  // of its 1 KB piece, so the source offset picks the global 16-byte piece
+  // that belongs at that swizzled position).
 #pragma unroll
-  for (int it = 0; it < (2 * NKI + 3) / 4; ++it) {
+  for (int it = 0; it < (NKI + 3) / 4; ++it) {
     const int m = wave + 4 * it;
-    if (m >= 2 * NKI) break;
-    const bool isq = m >= NKI;
-    const int mm = isq ? m - NKI : m;
-    const int u = 64 * mm + lane, row = u / KPR;
+    if (m >= NKI) break;
+    const int u = 64 * m + lane, row = u / KPR;
     const int gp = (u % KPR) ^ kn_swizzle<D>(row);
     const uint32_t off = (uint32_t)((row * hqk * D + 8 * gp) * 2);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(isq ? rq : rk, (lds_void *)((isq ? Qt : Kt) + 512 * mm),
-                                             16, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void *)(Kt + 512 * m), 16, off, 0, 0, 0);
+  }
+  // Q: only the B operand of Q K^T (and the Q fragments of the per-tile
+  // carry), so it goes straight into the registers of the two wavefronts
+  // that form Q K^T, in that operand's order: lane (l16, g4) of step s holds
+  // Q[16 ib + l16][32 s + 8 g4 + (0..7)]. Keeping it out of LDS halves the
+  // kernel's LDS, so more work-groups fit per CU.
+  const int prod = wave & 1;  // 0: K K^T, 1: Q K^T
+  const int rset = wave >> 1;
+  int rows[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) rows[r] = gram_row<NIB>(rset, r);
+  uint4 qv[2][F::DS];
+  if (prod) {
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+#pragma unroll
+      for (int s = 0; s < F::DS; ++s)
+        qv[r][s] = rows[r] < 0 ? make_uint4(0, 0, 0, 0)
+                               : buf_load_b128(rq, (uint32_t)(((16 * rows[r] + l16) * hqk * D +
+                                                               32 * s + 8 * g4) * 2));
+    }
   }
   // gamma: inclusive prefix sum of g over the chunk, lane t holding token t
   // (lanes past the end and past C hold g = 0: they repeat the last value).
@@ -227,43 +245,50 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
 
   // ---- for the per-tile carry (qfrag not null): Q of this chunk in the
   // A-operand order of Q S^T, block ib, step s, lane (l16, g4) holding
-  // Q[16 ib + l16][32 s + 8 g4 + (0..7)]. One value head of the group writes
-  // them.
-  if (gi == 0 && wave < NIB && qfrag != nullptr) {
+  // Q[16 ib + l16][32 s + 8 g4 + (0..7)]: the registers of the Q K^T
+  // wavefronts, which between them hold every block. One value head of the
+  // group writes them.
+  if (gi == 0 && prod && qfrag != nullptr) {
     const int64_t base = ((int64_t)cidx * hqk + hk) * (C * D);
-    uint16_t *qf = qfrag + base + ((int64_t)wave * F::DS * 64 + lane) * 8;
 #pragma unroll
-    for (int s = 0; s < F::DS; ++s)
-      *reinterpret_cast<uint4 *>(qf + s * 512) =
-          *reinterpret_cast<const uint4 *>(&Qt[kn_index<D>(16 * wave + l16, 32 * s + 8 * g4)]);
+    for (int r = 0; r < 2; ++r) {
+      if (rows[r] < 0) continue;
+      uint16_t *qf = qfrag + base + ((int64_t)rows[r] * F::DS * 64 + lane) * 8;
+#pragma unroll
+      for (int s = 0; s < F::DS; ++s) *reinterpret_cast<uint4 *>(qf + s * 512) = qv[r][s];
+    }
   }
 
   // ---- Gram tiles (ib, jb), jb <= ib, of this wavefront's product. Lane
   // (l16, g4) element e holds  k_j . k_i  (or  k_j . q_i),  j = 16 jb + 4 g4 + e,
   // i = 16 ib + l16.
-  const int prod = wave & 1;
-  const int rset = wave >> 1;
-  const uint16_t *Bt = prod ? Qt : Kt;
-  int rows[2];
   f32x4 G[2][NIB];
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
-    rows[r] = gram_row<NIB>(rset, r);
     const int ib = rows[r];
 #pragma unroll
     for (int jb = 0; jb < NIB; ++jb) {
       G[r][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
       if (jb > ib) continue;
+      if (prod) {
 #pragma unroll
-      for (int s = 0; s < F::DS; ++s) {
-        const int col = 32 * s + 8 * g4;
-        const uint4 a = *reinterpret_cast<const uint4 *>(&Kt[kn_index<D>(16 * jb + l16, col)]);
-        const uint4 bb = *reinterpret_cast<const uint4 *>(&Bt[kn_index<D>(16 * ib + l16, col)]);
-        G[r][jb] = mfma_16x16x32(a, bb, G[r][jb]);
+        for (int s = 0; s < F::DS; ++s) {
+          const uint4 a =
+              *reinterpret_cast<const uint4 *>(&Kt[kn_index<D>(16 * jb + l16, 32 * s + 8 * g4)]);
+          G[r][jb] = mfma_16x16x32(a, qv[r][s], G[r][jb]);
+        }
+      } else {
+#pragma unroll
+        for (int s = 0; s < F::DS; ++s) {
+          const int col = 32 * s + 8 * g4;
+          const uint4 a = *reinterpret_cast<const uint4 *>(&Kt[kn_index<D>(16 * jb + l16, col)]);
+          const uint4 bb = *reinterpret_cast<const uint4 *>(&Kt[kn_index<D>(16 * ib + l16, col)]);
+          G[r][jb] = mfma_16x16x32(a, bb, G[r][jb]);
+        }
       }
     }
   }
-  lds_barrier();  // the K and Q tiles are dead; the space is reused below
+  lds_barrier();  // the K tile is dead; the space is reused below
 
   // ---- decay masks: A (product 0) to LDS, P (product 1) to global.
   float *gw = L.u.inv.gam[wave], *bw = L.u.inv.bet[wave];
