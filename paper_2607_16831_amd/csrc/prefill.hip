@@ -29,6 +29,7 @@
 // Every exponent is a non-positive difference (for g <= 0), masked before
 // exp, so strongly decaying inputs cannot overflow.
 #include <algorithm>
+#include <type_traits>
 
 #include "gdn_launch.h"
 #include "prefill_common.h"
@@ -66,10 +67,10 @@ struct LocalLds {
     struct {
       float A[NBLK][16 * AP];     // block (m, c) at m (m + 1) / 2 + c, row-major
       float linv[NIB][16 * 17];   // transposed diagonal inverses
-      float gam[4][64];           // per-wavefront copies of gamma and beta
-      float bet[4][64];
     } inv;
   } u;
+  float gam[4][64];  // per-wavefront copies of gamma and beta
+  float bet[4][64];
 };
 
 // Block rows of row set p (one row set per pair of wavefronts): the longest
@@ -78,6 +79,96 @@ template <int NIB>
 __device__ __forceinline__ int gram_row(int p, int r) {
   if (r == 0) return NIB - 1 - p;
   return NIB == 4 ? p : -1;
+}
+
+// Block row IB of both Gram products and their decay masks, for wavefront
+// IB: first Q K^T, masked and stored as P fragments to global memory, then
+// K K^T, whose masked tiles become the A blocks of row IB once the K tile's
+// space is free (after the first of the two barriers every wavefront
+// passes). Lane (l16, g4) element e of a tile holds k_j . q_i (or
+// k_j . k_i), j = 16 jb + 4 g4 + e, i = 16 IB + l16. The row is a template
+// parameter so that only the tiles on or below the diagonal exist, and each
+// tile's K rows are read right before its products, which keeps a
+// wavefront's registers within what eight wavefronts per SIMD allow.
+template <int D, int C, int IB, typename LL>
+__device__ __forceinline__ void gram_row_masks(LL &L, const uint16_t *Kt, const uint4 (&qv)[D / 32],
+                                               const float *gw, const float *bw,
+                                               uint16_t *pf_base, int lane) {
+  using F = Cfg<D, C>;
+  constexpr int KS = F::KS, DS = F::DS, AP = LL::AP;
+  const int l16 = lane & 15, g4 = lane >> 4;
+  const int i = 16 * IB + l16;
+  auto masked = [&](int jb, const f32x4 &g, bool isp) {
+    const float gami = gw[i], bi = bw[i];
+    const float4 gj = *reinterpret_cast<const float4 *>(&gw[16 * jb + 4 * g4]);
+    const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
+    f32x4 m;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int j = 16 * jb + 4 * g4 + e;
+      const float dec = (j <= i) ? __expf(gami - gjv[e]) : 0.f;
+      m[e] = isp ? dec * g[e] : ((j < i) ? bi * dec * g[e] : 0.f);
+    }
+    return m;
+  };
+  // K rows of block jb, step s. The lane id passes through an empty asm at
+  // every read: otherwise the compiler computes every (jb, s) address up
+  // front and holds them all in registers.
+  auto krow = [&](int jb, int s) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    return *reinterpret_cast<const uint4 *>(
+        &Kt[kn_index<D>(16 * jb + (ln & 15), 32 * s + 8 * (ln >> 4))]);
+  };
+  if constexpr (IB < F::NIB) {
+    // ---- Q K^T and P
+    f32x4 Pt[IB + 1];
+#pragma unroll
+    for (int jb = 0; jb <= IB; ++jb) {
+      __builtin_amdgcn_sched_barrier(0);
+      Pt[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < DS; ++s) Pt[jb] = mfma_16x16x32(krow(jb, s), qv[s], Pt[jb]);
+    }
+#pragma unroll
+    for (int jb = 0; jb <= IB; ++jb) Pt[jb] = masked(jb, Pt[jb], true);
+    // P as A-operand fragments: step s takes tile 2s (elements 0-3) and tile
+    // 2s+1 (elements 4-7), i.e. the token order of tok_pos().
+    uint16_t *pf = pf_base + ((int64_t)IB * KS * 64 + lane) * 8;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      if (2 * s > IB) continue;  // above the diagonal: zero, never stored or read
+      const f32x4 lo4 = Pt[2 * s];
+      const f32x4 hi4 = (2 * s + 1 <= IB) ? Pt[(2 * s + 1) % (IB + 1)] : f32x4{0.f, 0.f, 0.f, 0.f};
+      *reinterpret_cast<uint4 *>(pf + s * 512) =
+          make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
+                     pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
+    }
+    // ---- K K^T (the B operand, K rows of block IB, read once)
+    __builtin_amdgcn_sched_barrier(0);
+    uint4 kb[DS];
+#pragma unroll
+    for (int s = 0; s < DS; ++s) kb[s] = krow(IB, s);
+    f32x4 G[IB + 1];
+#pragma unroll
+    for (int jb = 0; jb <= IB; ++jb) {
+      __builtin_amdgcn_sched_barrier(0);
+      G[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < DS; ++s) G[jb] = mfma_16x16x32(krow(jb, s), kb[s], G[jb]);
+    }
+    lds_barrier();  // the K tile is dead; the space is reused for A
+#pragma unroll
+    for (int jb = 0; jb <= IB; ++jb) {
+      const f32x4 m = masked(jb, G[jb], false);
+      *reinterpret_cast<float4 *>(&L.u.inv.A[IB * (IB + 1) / 2 + jb][l16 * AP + 4 * g4]) =
+          make_float4(m[0], m[1], m[2], m[3]);
+    }
+    lds_barrier();
+  } else {
+    lds_barrier();
+    lds_barrier();
+  }
 }
 
 // Inverse of one unit lower-triangular 16 x 16 block I + N by the Neumann
@@ -119,7 +210,7 @@ __device__ __forceinline__ f32x4 neumann_diag(const float *Ab, int g4, int l16) 
 }
 
 template <int D, int C, typename TIn, bool NEUMANN>
-__global__ __launch_bounds__(256) void chunk_local_kernel(
+__global__ __launch_bounds__(256, 8) void chunk_local_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k,
     const float *__restrict__ g, const float *__restrict__ beta, GateArgs gate,
     const int32_t *__restrict__ cu, int n_seqs, int hqk, int hv, int group,
@@ -211,26 +302,16 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void *)(Kt + 512 * m), 16, off, 0, 0, 0);
   }
   // Q: only the B operand of Q K^T (and the Q fragments of the per-tile
-  // carry), so it goes straight into the registers of the two wavefronts
-  // that form Q K^T, in that operand's order: lane (l16, g4) of step s holds
-  // Q[16 ib + l16][32 s + 8 g4 + (0..7)]. Keeping it out of LDS halves the
-  // kernel's LDS, so more work-groups fit per CU.
-  const int prod = wave & 1;  // 0: K K^T, 1: Q K^T
-  const int rset = wave >> 1;
-  int rows[2];
+  // carry), so it goes straight into registers: wavefront w holds block row
+  // w (when the chunk has one), in that operand's order: lane (l16, g4) of
+  // step s holds Q[16 w + l16][32 s + 8 g4 + (0..7)]. Keeping it out of LDS
+  // halves the kernel's LDS, so more work-groups fit per CU.
+  const bool qrow = wave < NIB;
+  uint4 qv[F::DS];
 #pragma unroll
-  for (int r = 0; r < 2; ++r) rows[r] = gram_row<NIB>(rset, r);
-  uint4 qv[2][F::DS];
-  if (prod) {
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-#pragma unroll
-      for (int s = 0; s < F::DS; ++s)
-        qv[r][s] = rows[r] < 0 ? make_uint4(0, 0, 0, 0)
-                               : buf_load_b128(rq, (uint32_t)(((16 * rows[r] + l16) * hqk * D +
-                                                               32 * s + 8 * g4) * 2));
-    }
-  }
+  for (int s = 0; s < F::DS; ++s)
+    qv[s] = qrow ? buf_load_b128(rq, (uint32_t)(((16 * wave + l16) * hqk * D + 32 * s + 8 * g4) * 2))
+                 : make_uint4(0, 0, 0, 0);
   // gamma: inclusive prefix sum of g over the chunk, lane t holding token t
   // (lanes past the end and past C hold g = 0: they repeat the last value).
   const float gam = wave_prefix_sum(gl);
@@ -240,100 +321,37 @@ __global__ __launch_bounds__(256) void chunk_local_kernel(
     dec_ws[slot * 2 * C + lane] = __expf(gam);
     dec_ws[slot * 2 * C + C + lane] = __expf(glast - gam);
   }
+  // per-wavefront copies of gamma and beta for the decay masks (outside the
+  // K tile's space: the Q K^T wavefronts mask before the tile is released)
+  float *gw = L.gam[wave], *bw = L.bet[wave];
+  gw[lane] = gam;
+  bw[lane] = bta;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
   // ---- for the per-tile carry (qfrag not null): Q of this chunk in the
   // A-operand order of Q S^T, block ib, step s, lane (l16, g4) holding
-  // Q[16 ib + l16][32 s + 8 g4 + (0..7)]: the registers of the Q K^T
-  // wavefronts, which between them hold every block. One value head of the
-  // group writes them.
-  if (gi == 0 && prod && qfrag != nullptr) {
+  // Q[16 ib + l16][32 s + 8 g4 + (0..7)]: the registers of wavefront ib. One
+  // value head of the group writes them.
+  if (gi == 0 && qrow && qfrag != nullptr) {
     const int64_t base = ((int64_t)cidx * hqk + hk) * (C * D);
+    uint16_t *qf = qfrag + base + ((int64_t)wave * F::DS * 64 + lane) * 8;
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      if (rows[r] < 0) continue;
-      uint16_t *qf = qfrag + base + ((int64_t)rows[r] * F::DS * 64 + lane) * 8;
-#pragma unroll
-      for (int s = 0; s < F::DS; ++s) *reinterpret_cast<uint4 *>(qf + s * 512) = qv[r][s];
-    }
+    for (int s = 0; s < F::DS; ++s) *reinterpret_cast<uint4 *>(qf + s * 512) = qv[s];
   }
 
-  // ---- Gram tiles (ib, jb), jb <= ib, of this wavefront's product. Lane
-  // (l16, g4) element e holds  k_j . k_i  (or  k_j . q_i),  j = 16 jb + 4 g4 + e,
-  // i = 16 ib + l16.
-  f32x4 G[2][NIB];
-#pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int ib = rows[r];
-#pragma unroll
-    for (int jb = 0; jb < NIB; ++jb) {
-      G[r][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (jb > ib) continue;
-      if (prod) {
-#pragma unroll
-        for (int s = 0; s < F::DS; ++s) {
-          const uint4 a =
-              *reinterpret_cast<const uint4 *>(&Kt[kn_index<D>(16 * jb + l16, 32 * s + 8 * g4)]);
-          G[r][jb] = mfma_16x16x32(a, qv[r][s], G[r][jb]);
-        }
-      } else {
-#pragma unroll
-        for (int s = 0; s < F::DS; ++s) {
-          const int col = 32 * s + 8 * g4;
-          const uint4 a = *reinterpret_cast<const uint4 *>(&Kt[kn_index<D>(16 * jb + l16, col)]);
-          const uint4 bb = *reinterpret_cast<const uint4 *>(&Kt[kn_index<D>(16 * ib + l16, col)]);
-          G[r][jb] = mfma_16x16x32(a, bb, G[r][jb]);
-        }
-      }
-    }
+  // ---- Gram tiles and decay masks: block row `wave` of both products
+  {
+    uint16_t *pfb = pfrag + slot * F::FRAG;
+    if (wave == 0)
+      gram_row_masks<D, C, 0>(L, Kt, qv, gw, bw, pfb, lane);
+    else if (wave == 1)
+      gram_row_masks<D, C, 1>(L, Kt, qv, gw, bw, pfb, lane);
+    else if (wave == 2)
+      gram_row_masks<D, C, 2>(L, Kt, qv, gw, bw, pfb, lane);
+    else
+      gram_row_masks<D, C, 3>(L, Kt, qv, gw, bw, pfb, lane);
   }
-  lds_barrier();  // the K tile is dead; the space is reused below
-
-  // ---- decay masks: A (product 0) to LDS, P (product 1) to global.
-  float *gw = L.u.inv.gam[wave], *bw = L.u.inv.bet[wave];
-  gw[lane] = gam;
-  bw[lane] = bta;
-  wave_lds_fence();
-#pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int ib = rows[r];
-    if (ib < 0) continue;
-    const int i = 16 * ib + l16;
-    const float gami = gw[i], bi = bw[i];
-    f32x4 Pt[NIB];
-#pragma unroll
-    for (int jb = 0; jb < NIB; ++jb) {
-      Pt[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (jb > ib) continue;
-      const float4 gj = *reinterpret_cast<const float4 *>(&gw[16 * jb + 4 * g4]);
-      const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int j = 16 * jb + 4 * g4 + e;
-        const float dec = (j <= i) ? __expf(gami - gjv[e]) : 0.f;
-        Pt[jb][e] = prod ? dec * G[r][jb][e] : ((j < i) ? bi * dec * G[r][jb][e] : 0.f);
-      }
-      if (!prod)
-        *reinterpret_cast<float4 *>(&L.u.inv.A[ib * (ib + 1) / 2 + jb][l16 * AP + 4 * g4]) =
-            make_float4(Pt[jb][0], Pt[jb][1], Pt[jb][2], Pt[jb][3]);
-    }
-    if (prod) {
-      // P as A-operand fragments: step s takes tile 2s (elements 0-3) and
-      // tile 2s+1 (elements 4-7), i.e. the token order of tok_pos().
-      uint16_t *pf = pfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        if (2 * s > ib) continue;  // above the diagonal: zero, never stored or read
-        const f32x4 lo4 = Pt[2 * s];
-        const f32x4 hi4 = (2 * s + 1 < NIB) ? Pt[(2 * s + 1) % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
-        *reinterpret_cast<uint4 *>(pf + s * 512) =
-            make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
-                       pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
-      }
-    }
-  }
-  lds_barrier();
 
   // ---- diagonal blocks. Neumann product: wavefront b inverts block b and
   // stores it transposed (linv[b] row c = column c of the inverse).
