@@ -46,8 +46,8 @@ namespace gdn {
 // the same XCD so that the second reads K and Q from its L2.
 //
 // The 16x16 tiles of the two lower-triangular Gram products are dealt out
-// evenly: wavefront w computes product (w & 1) (0: K K^T for A, 1: K Q^T
-// for P) for the block rows of row set (w >> 1).
+// evenly: wavefront w computes block row w of Q K^T (its Q rows are in its
+// registers) and block row NIB - 1 - w of K K^T, NIB + 1 tiles each.
 //
 // T is built from its 16x16 blocks in fp32. Diagonal block b is inverted
 // either by forward substitution on the vector ALU (one lane per column, all
@@ -73,32 +73,26 @@ struct LocalLds {
   float bet[4][64];
 };
 
-// Block rows of row set p (one row set per pair of wavefronts): the longest
-// row with the shortest, so that every set holds the same number of tiles.
-template <int NIB>
-__device__ __forceinline__ int gram_row(int p, int r) {
-  if (r == 0) return NIB - 1 - p;
-  return NIB == 4 ? p : -1;
-}
-
-// Block row IB of both Gram products and their decay masks, for wavefront
-// IB: first Q K^T, masked and stored as P fragments to global memory, then
-// K K^T, whose masked tiles become the A blocks of row IB once the K tile's
-// space is free (after the first of the two barriers every wavefront
-// passes). Lane (l16, g4) element e of a tile holds k_j . q_i (or
-// k_j . k_i), j = 16 jb + 4 g4 + e, i = 16 IB + l16. The row is a template
-// parameter so that only the tiles on or below the diagonal exist, and each
-// tile's K rows are read right before its products, which keeps a
-// wavefront's registers within what eight wavefronts per SIMD allow.
-template <int D, int C, int IB, typename LL>
+// Block row QB of Q K^T and block row KB of K K^T with their decay masks,
+// for one wavefront: first Q K^T, masked and stored as P fragments to global
+// memory, then K K^T, whose masked tiles become the A blocks of row KB once
+// the K tile's space is free (after the first of the two barriers every
+// wavefront passes). Wavefront w takes QB = w (its Q registers) and
+// KB = NIB - 1 - w, so that every wavefront forms NIB + 1 tiles. Lane
+// (l16, g4) element e of a tile holds k_j . q_i (or k_j . k_i),
+// j = 16 jb + 4 g4 + e, i = 16 (row) + l16. The rows are template parameters
+// so that only the tiles on or below the diagonal exist, and each tile's K
+// rows are read right before its products, which keeps a wavefront's
+// registers within what eight wavefronts per SIMD allow.
+template <int D, int C, int QB, int KB, typename LL>
 __device__ __forceinline__ void gram_row_masks(LL &L, const uint16_t *Kt, const uint4 (&qv)[D / 32],
                                                const float *gw, const float *bw,
                                                uint16_t *pf_base, int lane) {
   using F = Cfg<D, C>;
   constexpr int KS = F::KS, DS = F::DS, AP = LL::AP;
   const int l16 = lane & 15, g4 = lane >> 4;
-  const int i = 16 * IB + l16;
-  auto masked = [&](int jb, const f32x4 &g, bool isp) {
+  auto masked = [&](int ib, int jb, const f32x4 &g, bool isp) {
+    const int i = 16 * ib + l16;
     const float gami = gw[i], bi = bw[i];
     const float4 gj = *reinterpret_cast<const float4 *>(&gw[16 * jb + 4 * g4]);
     const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
@@ -120,38 +114,38 @@ __device__ __forceinline__ void gram_row_masks(LL &L, const uint16_t *Kt, const 
     return *reinterpret_cast<const uint4 *>(
         &Kt[kn_index<D>(16 * jb + (ln & 15), 32 * s + 8 * (ln >> 4))]);
   };
-  if constexpr (IB < F::NIB) {
+  if constexpr (QB < F::NIB) {
     // ---- Q K^T and P
-    f32x4 Pt[IB + 1];
+    f32x4 Pt[QB + 1];
 #pragma unroll
-    for (int jb = 0; jb <= IB; ++jb) {
+    for (int jb = 0; jb <= QB; ++jb) {
       __builtin_amdgcn_sched_barrier(0);
       Pt[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < DS; ++s) Pt[jb] = mfma_16x16x32(krow(jb, s), qv[s], Pt[jb]);
     }
 #pragma unroll
-    for (int jb = 0; jb <= IB; ++jb) Pt[jb] = masked(jb, Pt[jb], true);
+    for (int jb = 0; jb <= QB; ++jb) Pt[jb] = masked(QB, jb, Pt[jb], true);
     // P as A-operand fragments: step s takes tile 2s (elements 0-3) and tile
     // 2s+1 (elements 4-7), i.e. the token order of tok_pos().
-    uint16_t *pf = pf_base + ((int64_t)IB * KS * 64 + lane) * 8;
+    uint16_t *pf = pf_base + ((int64_t)QB * KS * 64 + lane) * 8;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      if (2 * s > IB) continue;  // above the diagonal: zero, never stored or read
+      if (2 * s > QB) continue;  // above the diagonal: zero, never stored or read
       const f32x4 lo4 = Pt[2 * s];
-      const f32x4 hi4 = (2 * s + 1 <= IB) ? Pt[(2 * s + 1) % (IB + 1)] : f32x4{0.f, 0.f, 0.f, 0.f};
+      const f32x4 hi4 = (2 * s + 1 <= QB) ? Pt[(2 * s + 1) % (QB + 1)] : f32x4{0.f, 0.f, 0.f, 0.f};
       *reinterpret_cast<uint4 *>(pf + s * 512) =
           make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
                      pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
     }
-    // ---- K K^T (the B operand, K rows of block IB, read once)
+    // ---- K K^T (the B operand, K rows of block KB, read once)
     __builtin_amdgcn_sched_barrier(0);
     uint4 kb[DS];
 #pragma unroll
-    for (int s = 0; s < DS; ++s) kb[s] = krow(IB, s);
-    f32x4 G[IB + 1];
+    for (int s = 0; s < DS; ++s) kb[s] = krow(KB, s);
+    f32x4 G[KB + 1];
 #pragma unroll
-    for (int jb = 0; jb <= IB; ++jb) {
+    for (int jb = 0; jb <= KB; ++jb) {
       __builtin_amdgcn_sched_barrier(0);
       G[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -159,9 +153,9 @@ __device__ __forceinline__ void gram_row_masks(LL &L, const uint16_t *Kt, const 
     }
     lds_barrier();  // the K tile is dead; the space is reused for A
 #pragma unroll
-    for (int jb = 0; jb <= IB; ++jb) {
-      const f32x4 m = masked(jb, G[jb], false);
-      *reinterpret_cast<float4 *>(&L.u.inv.A[IB * (IB + 1) / 2 + jb][l16 * AP + 4 * g4]) =
+    for (int jb = 0; jb <= KB; ++jb) {
+      const f32x4 m = masked(KB, jb, G[jb], false);
+      *reinterpret_cast<float4 *>(&L.u.inv.A[KB * (KB + 1) / 2 + jb][l16 * AP + 4 * g4]) =
           make_float4(m[0], m[1], m[2], m[3]);
     }
     lds_barrier();
@@ -340,17 +334,18 @@ __global__ __launch_bounds__(256, 8) void chunk_local_kernel(
     for (int s = 0; s < F::DS; ++s) *reinterpret_cast<uint4 *>(qf + s * 512) = qv[s];
   }
 
-  // ---- Gram tiles and decay masks: block row `wave` of both products
+  // ---- Gram tiles and decay masks: row `wave` of Q K^T, row NIB-1-wave of K K^T
   {
     uint16_t *pfb = pfrag + slot * F::FRAG;
+    constexpr int M = NIB - 1;  // K K^T row of wavefront w: M - w
     if (wave == 0)
-      gram_row_masks<D, C, 0>(L, Kt, qv, gw, bw, pfb, lane);
+      gram_row_masks<D, C, 0, M>(L, Kt, qv, gw, bw, pfb, lane);
     else if (wave == 1)
-      gram_row_masks<D, C, 1>(L, Kt, qv, gw, bw, pfb, lane);
+      gram_row_masks<D, C, 1, (M >= 1 ? M - 1 : 0)>(L, Kt, qv, gw, bw, pfb, lane);
     else if (wave == 2)
-      gram_row_masks<D, C, 2>(L, Kt, qv, gw, bw, pfb, lane);
+      gram_row_masks<D, C, 2, (M >= 2 ? M - 2 : 0)>(L, Kt, qv, gw, bw, pfb, lane);
     else
-      gram_row_masks<D, C, 3>(L, Kt, qv, gw, bw, pfb, lane);
+      gram_row_masks<D, C, 3, (M >= 3 ? M - 3 : 0)>(L, Kt, qv, gw, bw, pfb, lane);
   }
 
   // ---- diagonal blocks. Neumann product: wavefront b inverts block b and
