@@ -57,7 +57,9 @@ namespace gdn {
 //   T[b][c] = -(sum_{m=c+1..b} T[b][m] A[m][c]) T[c][c]^-1    (c < b),
 // carried in transposed form so that every intermediate stays in the
 // accumulator layout of the fp32 16x16x4 matrix instruction.
-template <int D, int C>
+// HPW value heads per work-group (1 or 2): each head has its own A blocks,
+// inverses and gate copies; the K tile and the Gram products are shared.
+template <int D, int C, int HPW>
 struct LocalLds {
   static constexpr int NIB = C / 16;
   static constexpr int NBLK = NIB * (NIB + 1) / 2;  // lower blocks, diagonal included
@@ -65,33 +67,36 @@ struct LocalLds {
   union {
     uint16_t kq[C * D];  // K tile, swizzled rows (kn_index)
     struct {
-      float A[NBLK][16 * AP];     // block (m, c) at m (m + 1) / 2 + c, row-major
-      float linv[NIB][16 * 17];   // transposed diagonal inverses
+      float A[HPW][NBLK][16 * AP];    // block (m, c) at m (m + 1) / 2 + c, row-major
+      float linv[HPW][NIB][16 * 17];  // transposed diagonal inverses
     } inv;
   } u;
-  float gam[4][64];  // per-wavefront copies of gamma and beta
-  float bet[4][64];
+  float gam[HPW][4][64];  // per-wavefront copies of gamma and beta
+  float bet[HPW][4][64];
 };
 
 // Block row QB of Q K^T and block row KB of K K^T with their decay masks,
-// for one wavefront: first Q K^T, masked and stored as P fragments to global
-// memory, then K K^T, whose masked tiles become the A blocks of row KB once
-// the K tile's space is free (after the first of the two barriers every
-// wavefront passes). Wavefront w takes QB = w (its Q registers) and
-// KB = NIB - 1 - w, so that every wavefront forms NIB + 1 tiles. Lane
-// (l16, g4) element e of a tile holds k_j . q_i (or k_j . k_i),
-// j = 16 jb + 4 g4 + e, i = 16 (row) + l16. The rows are template parameters
-// so that only the tiles on or below the diagonal exist, and each tile's K
-// rows are read right before its products, which keeps a wavefront's
-// registers within what eight wavefronts per SIMD allow.
-template <int D, int C, int QB, int KB, typename LL>
+// for one wavefront: first Q K^T, masked with each head's gates and stored
+// as P fragments to global memory, then K K^T, whose masked tiles become
+// each head's A blocks of row KB once the K tile's space is free (after the
+// first of the two barriers every wavefront passes). The products depend
+// only on the key head, so the HPW heads of the work-group share them.
+// Wavefront w takes QB = w (its Q registers) and KB = NIB - 1 - w, so that
+// every wavefront forms NIB + 1 tiles. Lane (l16, g4) element e of a tile
+// holds k_j . q_i (or k_j . k_i), j = 16 jb + 4 g4 + e, i = 16 (row) + l16.
+// The rows are template parameters so that only the tiles on or below the
+// diagonal exist, and each tile's K rows are read right before its
+// products, which keeps a wavefront's registers within what its occupancy
+// allows.
+template <int D, int C, int HPW, int QB, int KB, typename LL>
 __device__ __forceinline__ void gram_row_masks(LL &L, const uint16_t *Kt, const uint4 (&qv)[D / 32],
-                                               const float *gw, const float *bw,
-                                               uint16_t *pf_base, int lane) {
+                                               int wave, uint16_t *const (&pf_base)[HPW],
+                                               int lane) {
   using F = Cfg<D, C>;
   constexpr int KS = F::KS, DS = F::DS, AP = LL::AP;
   const int l16 = lane & 15, g4 = lane >> 4;
-  auto masked = [&](int ib, int jb, const f32x4 &g, bool isp) {
+  auto masked = [&](int hh, int ib, int jb, const f32x4 &g, bool isp) {
+    const float *gw = L.gam[hh][wave], *bw = L.bet[hh][wave];
     const int i = 16 * ib + l16;
     const float gami = gw[i], bi = bw[i];
     const float4 gj = *reinterpret_cast<const float4 *>(&gw[16 * jb + 4 * g4]);
@@ -124,19 +129,22 @@ __device__ __forceinline__ void gram_row_masks(LL &L, const uint16_t *Kt, const 
 #pragma unroll
       for (int s = 0; s < DS; ++s) Pt[jb] = mfma_16x16x32(krow(jb, s), qv[s], Pt[jb]);
     }
-#pragma unroll
-    for (int jb = 0; jb <= QB; ++jb) Pt[jb] = masked(QB, jb, Pt[jb], true);
     // P as A-operand fragments: step s takes tile 2s (elements 0-3) and tile
     // 2s+1 (elements 4-7), i.e. the token order of tok_pos().
-    uint16_t *pf = pf_base + ((int64_t)QB * KS * 64 + lane) * 8;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      if (2 * s > QB) continue;  // above the diagonal: zero, never stored or read
-      const f32x4 lo4 = Pt[2 * s];
-      const f32x4 hi4 = (2 * s + 1 <= QB) ? Pt[(2 * s + 1) % (QB + 1)] : f32x4{0.f, 0.f, 0.f, 0.f};
-      *reinterpret_cast<uint4 *>(pf + s * 512) =
-          make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
-                     pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
+    for (int hh = 0; hh < HPW; ++hh) {
+      uint16_t *pf = pf_base[hh] + ((int64_t)QB * KS * 64 + lane) * 8;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        if (2 * s > QB) continue;  // above the diagonal: zero, never stored or read
+        const f32x4 lo4 = masked(hh, QB, 2 * s, Pt[2 * s], true);
+        const f32x4 hi4 = (2 * s + 1 <= QB)
+                              ? masked(hh, QB, 2 * s + 1, Pt[(2 * s + 1) % (QB + 1)], true)
+                              : f32x4{0.f, 0.f, 0.f, 0.f};
+        *reinterpret_cast<uint4 *>(pf + s * 512) =
+            make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
+                       pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
+      }
     }
     // ---- K K^T (the B operand, K rows of block KB, read once)
     __builtin_amdgcn_sched_barrier(0);
@@ -153,10 +161,13 @@ __device__ __forceinline__ void gram_row_masks(LL &L, const uint16_t *Kt, const 
     }
     lds_barrier();  // the K tile is dead; the space is reused for A
 #pragma unroll
-    for (int jb = 0; jb <= KB; ++jb) {
-      const f32x4 m = masked(KB, jb, G[jb], false);
-      *reinterpret_cast<float4 *>(&L.u.inv.A[KB * (KB + 1) / 2 + jb][l16 * AP + 4 * g4]) =
-          make_float4(m[0], m[1], m[2], m[3]);
+    for (int hh = 0; hh < HPW; ++hh) {
+#pragma unroll
+      for (int jb = 0; jb <= KB; ++jb) {
+        const f32x4 m = masked(hh, KB, jb, G[jb], false);
+        *reinterpret_cast<float4 *>(&L.u.inv.A[hh][KB * (KB + 1) / 2 + jb][l16 * AP + 4 * g4]) =
+            make_float4(m[0], m[1], m[2], m[3]);
+      }
     }
     lds_barrier();
   } else {
@@ -203,16 +214,17 @@ __device__ __forceinline__ f32x4 neumann_diag(const float *Ab, int g4, int l16) 
   return inv;
 }
 
-template <int D, int C, typename TIn, bool NEUMANN>
-__global__ __launch_bounds__(256, 8) void chunk_local_kernel(
+template <int D, int C, typename TIn, bool NEUMANN, int HPW>
+__global__ __launch_bounds__(256, HPW == 1 ? 8 : 4) void chunk_local_kernel(
     const TIn *__restrict__ q, const TIn *__restrict__ k,
     const float *__restrict__ g, const float *__restrict__ beta, GateArgs gate,
     const int32_t *__restrict__ cu, int n_seqs, int hqk, int hv, int group,
     int n_pairs, float *__restrict__ dec_ws, uint16_t *__restrict__ tfrag,
     uint16_t *__restrict__ pfrag, uint16_t *__restrict__ qfrag) {
   static_assert(sizeof(TIn) == 2, "bf16 inputs (float32 inputs take prefill_f32.hip)");
+  static_assert(HPW == 1 || HPW == 2, "heads per work-group");
   using F = Cfg<D, C>;
-  using LL = LocalLds<D, C>;
+  using LL = LocalLds<D, C, HPW>;
   constexpr int NIB = F::NIB, KS = F::KS, AP = LL::AP;
   constexpr int NKI = C * D / 512;  // 1 KB pieces of the K (or Q) tile
   constexpr int KPR = D / 8;        // 16-byte pieces per row
@@ -220,17 +232,19 @@ __global__ __launch_bounds__(256, 8) void chunk_local_kernel(
   __shared__ __attribute__((aligned(16))) LL L;
   uint16_t *Kt = L.u.kq;
 
-  // Block id -> (chunk, key head) pair and head of the group. Work-groups are
-  // dealt to the eight XCDs round robin, so ids b and b + 8 share one: the
-  // heads of a group for one pair take ids 8 (group j + gi) + x.
+  // Block id -> (chunk, key head) pair and set of HPW heads of the group.
+  // Work-groups are dealt to the eight XCDs round robin, so ids b and b + 8
+  // share one: the head sets of a group for one pair take ids
+  // 8 (nsets j + gi) + x.
+  const int nsets = group / HPW;
   const int bid = blockIdx.x;
   const int xg = bid & 7, jj = bid >> 3;
-  const int gi = jj % group;
-  const int pair = (jj / group) * 8 + xg;
+  const int gi = jj % nsets;
+  const int pair = (jj / nsets) * 8 + xg;
   if (pair >= n_pairs) return;
   const int cidx = pair / hqk, hk = pair - cidx * hqk;
-  const int h = hk * group + gi;
-  const int64_t slot = (int64_t)cidx * hv + h;
+  const int h0 = hk * group + gi * HPW;  // heads h0 .. h0 + HPW - 1
+  const int64_t slot0 = (int64_t)cidx * hv + h0;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
@@ -266,22 +280,26 @@ __global__ __launch_bounds__(256, 8) void chunk_local_kernel(
   const uint32_t rowb = (uint32_t)(nvalid * hqk * D * sizeof(TIn));
   const rsrc_t rk = make_rsrc(k + (t0 * hqk + hk) * D, rowb);
   const rsrc_t rq = make_rsrc(q + (t0 * hqk + hk) * D, rowb);
-  // g and beta of token `lane` (0 past the end), read or formed from the raw
-  // gate inputs
-  float gl, bta;
-  if (gate.a_log != nullptr) {  // uniform over the launch
-    const rsrc_t ra = make_rsrc(gate.a + t0 * hv, (uint32_t)(nvalid * hv * 4));
-    const rsrc_t rb = make_rsrc(gate.b + t0 * hv, (uint32_t)(nvalid * hv * 4));
-    const float ga = buf_load_f32(ra, (uint32_t)(lane * hv + h) * 4u);
-    const float gb = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
-    const bool in = lane < nvalid;
-    gl = in ? gate_log_decay(ga, gate.a_log[h], gate.dt_bias[h]) : 0.f;
-    bta = in ? gate_beta(gb) : 0.f;
-  } else {
-    const rsrc_t rg = make_rsrc(g + t0 * hv, (uint32_t)(nvalid * hv * 4));
-    const rsrc_t rb = make_rsrc(beta + t0 * hv, (uint32_t)(nvalid * hv * 4));
-    gl = buf_load_f32(rg, (uint32_t)(lane * hv + h) * 4u);
-    bta = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
+  // g and beta of token `lane` (0 past the end) for each head, read or
+  // formed from the raw gate inputs
+  float gl[HPW], bta[HPW];
+#pragma unroll
+  for (int hh = 0; hh < HPW; ++hh) {
+    const int h = h0 + hh;
+    if (gate.a_log != nullptr) {  // uniform over the launch
+      const rsrc_t ra = make_rsrc(gate.a + t0 * hv, (uint32_t)(nvalid * hv * 4));
+      const rsrc_t rb = make_rsrc(gate.b + t0 * hv, (uint32_t)(nvalid * hv * 4));
+      const float ga = buf_load_f32(ra, (uint32_t)(lane * hv + h) * 4u);
+      const float gb = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
+      const bool in = lane < nvalid;
+      gl[hh] = in ? gate_log_decay(ga, gate.a_log[h], gate.dt_bias[h]) : 0.f;
+      bta[hh] = in ? gate_beta(gb) : 0.f;
+    } else {
+      const rsrc_t rg = make_rsrc(g + t0 * hv, (uint32_t)(nvalid * hv * 4));
+      const rsrc_t rb = make_rsrc(beta + t0 * hv, (uint32_t)(nvalid * hv * 4));
+      gl[hh] = buf_load_f32(rg, (uint32_t)(lane * hv + h) * 4u);
+      bta[hh] = buf_load_f32(rb, (uint32_t)(lane * hv + h) * 4u);
+    }
   }
   // K: buffer-to-LDS copies (lane i of a copy fills bytes [16 i, 16 i + 16)
   // of its 1 KB piece, so the source offset picks the global 16-byte piece
@@ -308,18 +326,21 @@ __global__ __launch_bounds__(256, 8) void chunk_local_kernel(
                  : make_uint4(0, 0, 0, 0);
   // gamma: inclusive prefix sum of g over the chunk, lane t holding token t
   // (lanes past the end and past C hold g = 0: they repeat the last value).
-  const float gam = wave_prefix_sum(gl);
-  if (wave == 0 && lane < C) {
-    // decay factors for the carry: exp(gamma_i) and exp(gamma_last - gamma_i)
-    const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gam), C - 1));
-    dec_ws[slot * 2 * C + lane] = __expf(gam);
-    dec_ws[slot * 2 * C + C + lane] = __expf(glast - gam);
+#pragma unroll
+  for (int hh = 0; hh < HPW; ++hh) {
+    const float gam = wave_prefix_sum(gl[hh]);
+    if (wave == hh && lane < C) {
+      // decay factors for the carry: exp(gamma_i) and exp(gamma_last - gamma_i)
+      const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gam), C - 1));
+      const int64_t slot = slot0 + hh;
+      dec_ws[slot * 2 * C + lane] = __expf(gam);
+      dec_ws[slot * 2 * C + C + lane] = __expf(glast - gam);
+    }
+    // per-wavefront copies of gamma and beta for the decay masks (outside
+    // the K tile's space: Q K^T is masked before the tile is released)
+    L.gam[hh][wave][lane] = gam;
+    L.bet[hh][wave][lane] = bta[hh];
   }
-  // per-wavefront copies of gamma and beta for the decay masks (outside the
-  // K tile's space: the Q K^T wavefronts mask before the tile is released)
-  float *gw = L.gam[wave], *bw = L.bet[wave];
-  gw[lane] = gam;
-  bw[lane] = bta;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
@@ -327,7 +348,7 @@ __global__ __launch_bounds__(256, 8) void chunk_local_kernel(
   // A-operand order of Q S^T, block ib, step s, lane (l16, g4) holding
   // Q[16 ib + l16][32 s + 8 g4 + (0..7)]: the registers of wavefront ib. One
   // value head of the group writes them.
-  if (gi == 0 && qrow && qfrag != nullptr) {
+  if (gi == 0 && qrow && qfrag != nullptr) {  // one head set of the group
     const int64_t base = ((int64_t)cidx * hqk + hk) * (C * D);
     uint16_t *qf = qfrag + base + ((int64_t)wave * F::DS * 64 + lane) * 8;
 #pragma unroll
@@ -336,31 +357,37 @@ __global__ __launch_bounds__(256, 8) void chunk_local_kernel(
 
   // ---- Gram tiles and decay masks: row `wave` of Q K^T, row NIB-1-wave of K K^T
   {
-    uint16_t *pfb = pfrag + slot * F::FRAG;
+    uint16_t *pfb[HPW];
+#pragma unroll
+    for (int hh = 0; hh < HPW; ++hh) pfb[hh] = pfrag + (slot0 + hh) * F::FRAG;
     constexpr int M = NIB - 1;  // K K^T row of wavefront w: M - w
     if (wave == 0)
-      gram_row_masks<D, C, 0, M>(L, Kt, qv, gw, bw, pfb, lane);
+      gram_row_masks<D, C, HPW, 0, M>(L, Kt, qv, wave, pfb, lane);
     else if (wave == 1)
-      gram_row_masks<D, C, 1, (M >= 1 ? M - 1 : 0)>(L, Kt, qv, gw, bw, pfb, lane);
+      gram_row_masks<D, C, HPW, 1, (M >= 1 ? M - 1 : 0)>(L, Kt, qv, wave, pfb, lane);
     else if (wave == 2)
-      gram_row_masks<D, C, 2, (M >= 2 ? M - 2 : 0)>(L, Kt, qv, gw, bw, pfb, lane);
+      gram_row_masks<D, C, HPW, 2, (M >= 2 ? M - 2 : 0)>(L, Kt, qv, wave, pfb, lane);
     else
-      gram_row_masks<D, C, 3, (M >= 3 ? M - 3 : 0)>(L, Kt, qv, gw, bw, pfb, lane);
+      gram_row_masks<D, C, HPW, 3, (M >= 3 ? M - 3 : 0)>(L, Kt, qv, wave, pfb, lane);
   }
 
   // ---- diagonal blocks. Neumann product: wavefront b inverts block b and
   // stores it transposed (linv[b] row c = column c of the inverse).
   if (NEUMANN && wave < NIB) {
-    const f32x4 tb = neumann_diag<AP>(L.u.inv.A[wave * (wave + 1) / 2 + wave], g4, l16);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) L.u.inv.linv[wave][l16 * 17 + 4 * g4 + e] = tb[e];
+    for (int hh = 0; hh < HPW; ++hh) {
+      const f32x4 tb = neumann_diag<AP>(L.u.inv.A[hh][wave * (wave + 1) / 2 + wave], g4, l16);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) L.u.inv.linv[hh][wave][l16 * 17 + 4 * g4 + e] = tb[e];
+    }
   }
-  // Forward substitution: lane (b, c) = (g4, l16) solves (I + A[b][b]) x =
-  // e_c, i.e. column c of T[b][b], and stores it as row c of the transposed
-  // inverse.
-  if (!NEUMANN && wave == 0) {
+  // Forward substitution, wavefront hh for head hh: lane (b, c) = (g4, l16)
+  // solves (I + A[b][b]) x = e_c, i.e. column c of T[b][b], and stores it as
+  // row c of the transposed inverse.
+  if (!NEUMANN && wave < HPW) {
+    const int hh = wave;
     const int b = min(g4, NIB - 1);  // lanes past the last block repeat it
-    const float *Ab = L.u.inv.A[b * (b + 1) / 2 + b];
+    const float *Ab = L.u.inv.A[hh][b * (b + 1) / 2 + b];
     float x[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -375,21 +402,25 @@ __global__ __launch_bounds__(256, 8) void chunk_local_kernel(
     }
     if (g4 < NIB) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) L.u.inv.linv[b][l16 * 17 + i] = x[i];
+      for (int i = 0; i < 16; ++i) L.u.inv.linv[hh][b][l16 * 17 + i] = x[i];
     }
   }
   lds_barrier();
 
-  // ---- block row ib = wave, right to left: Z[c] = (T[ib][c])^T.
-  if (wave < NIB) {
+  // ---- block row ib = wave of each head, right to left: Z[c] = (T[ib][c])^T.
+#pragma unroll
+  for (int hh = 0; hh < HPW; ++hh) {
+    if (wave >= NIB) break;
     const int ib = wave;
+    const int64_t slot = slot0 + hh;
+    const float *bw = L.bet[hh][wave];
     f32x4 Z[NIB];
 #pragma unroll
     for (int c = 0; c < NIB; ++c) {
       Z[c] = f32x4{0.f, 0.f, 0.f, 0.f};
       if (c == ib) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) Z[c][e] = L.u.inv.linv[ib][(4 * g4 + e) * 17 + l16];
+        for (int e = 0; e < 4; ++e) Z[c][e] = L.u.inv.linv[hh][ib][(4 * g4 + e) * 17 + l16];
       }
     }
 #pragma unroll
@@ -399,7 +430,7 @@ __global__ __launch_bounds__(256, 8) void chunk_local_kernel(
 #pragma unroll
       for (int m = 1; m < NIB; ++m) {
         if (m <= c || m > ib) continue;
-        const float *Amc = L.u.inv.A[m * (m + 1) / 2 + c];
+        const float *Amc = L.u.inv.A[hh][m * (m + 1) / 2 + c];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk)
           R = mfma_16x16x4_f32(Amc[(4 * g4 + kk) * AP + l16], Z[m][kk], R);
@@ -407,7 +438,7 @@ __global__ __launch_bounds__(256, 8) void chunk_local_kernel(
       f32x4 Zc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk)
-        Zc = mfma_16x16x4_f32(L.u.inv.linv[c][l16 * 17 + 4 * g4 + kk], R[kk], Zc);
+        Zc = mfma_16x16x4_f32(L.u.inv.linv[hh][c][l16 * 17 + 4 * g4 + kk], R[kk], Zc);
       Z[c] = -Zc;
     }
     // Fold beta into the factor: the carry uses T' = T diag(beta), so that
@@ -716,9 +747,14 @@ static hipError_t launch_prefill_t(const PrefillArgs &a, const PrefillWorkspace 
   if (a.n_tokens > 0) {
     // (chunk, key head) pairs in groups of eight, times the heads of a group.
     const int64_t pairs = nc * a.hqk;
-    const int64_t lblocks = ((pairs + 7) / 8) * 8 * group;
-    auto local = a.neumann ? chunk_local_kernel<D, C, TIn, true>
-                           : chunk_local_kernel<D, C, TIn, false>;
+    // Two value heads per work-group when the group has an even size: they
+    // share the K tile and the Gram products.
+    const int hpw = (group % 2 == 0) ? 2 : 1;
+    const int64_t lblocks = ((pairs + 7) / 8) * 8 * (group / hpw);
+    auto local = hpw == 2 ? (a.neumann ? chunk_local_kernel<D, C, TIn, true, 2>
+                                       : chunk_local_kernel<D, C, TIn, false, 2>)
+                          : (a.neumann ? chunk_local_kernel<D, C, TIn, true, 1>
+                                       : chunk_local_kernel<D, C, TIn, false, 1>);
     hipLaunchKernelGGL(local, dim3((unsigned)lblocks), dim3(256), 0, a.stream, (const TIn *)a.q,
                        (const TIn *)a.k, a.g, a.beta, a.gate, a.cu_seqlens, a.n_seqs, a.hqk, a.hv,
                        group, (int)pairs, dec, tf, pf, qf);
