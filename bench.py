@@ -45,8 +45,8 @@ METRIC = "prefill tokens/sec + MFMA util; decode µs/step + achieved HBM GB/s"
 # the kernel sources they were taken on. Any change to those sources makes
 # the figures stale, and `traffic` is then reported as null.
 MEASURED_TRAFFIC = {
-    "08d95e40681111e45f0cbd5e8be7deab446377e1a5d77c4a0971fe709c5f9f63":
-        {"prefill": 225089750, "decode": 274399873},
+    "69b1b688c93a055dfa93db621486ea1ed0e58cd82e21e2f7cc4d03ab7d340c95":
+        {"prefill": 225154446, "decode": 274399456},
 }
 
 
