@@ -125,6 +125,18 @@ __device__ __forceinline__ float4 buf_load_f32x4(rsrc_t r, uint32_t off) {
 // Cache-policy operand of the buffer intrinsics: the non-temporal (streaming)
 // bit of gfx940-family targets (the position of SLC on earlier gfx9).
 constexpr int kCachePolicyNT = 2;
+// SC1 set, SC0 clear: a device-scope store on gfx940-family targets, written
+// through the XCD's L2 to the memory side that every XCD shares. For tables
+// that the next kernel reads on other XCDs it saves the write-back of dirty
+// L2 lines at the end of the kernel.
+constexpr int kCachePolicyDevice = 16;
+
+template <int POL>
+__device__ __forceinline__ void buf_store_b128(rsrc_t r, uint32_t off, uint4 v) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 x = {v.x, v.y, v.z, v.w};
+  __builtin_amdgcn_raw_buffer_store_b128(x, r, off, 0, POL);
+}
 
 // Element access through a buffer resource; offsets are in elements.
 template <typename T>

@@ -130,10 +130,11 @@ __device__ __forceinline__ void gram_row_masks(LL &L, const uint16_t *Kt, const 
       for (int s = 0; s < DS; ++s) Pt[jb] = mfma_16x16x32(krow(jb, s), qv[s], Pt[jb]);
     }
     // P as A-operand fragments: step s takes tile 2s (elements 0-3) and tile
-    // 2s+1 (elements 4-7), i.e. the token order of tok_pos().
+    // 2s+1 (elements 4-7), i.e. the token order of tok_pos(). Device-scope
+    // stores, like every table the carry reads.
 #pragma unroll
     for (int hh = 0; hh < HPW; ++hh) {
-      uint16_t *pf = pf_base[hh] + ((int64_t)QB * KS * 64 + lane) * 8;
+      const rsrc_t rpf = make_rsrc(pf_base[hh], F::FRAG * 2);
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         if (2 * s > QB) continue;  // above the diagonal: zero, never stored or read
@@ -141,9 +142,10 @@ __device__ __forceinline__ void gram_row_masks(LL &L, const uint16_t *Kt, const 
         const f32x4 hi4 = (2 * s + 1 <= QB)
                               ? masked(hh, QB, 2 * s + 1, Pt[(2 * s + 1) % (QB + 1)], true)
                               : f32x4{0.f, 0.f, 0.f, 0.f};
-        *reinterpret_cast<uint4 *>(pf + s * 512) =
+        buf_store_b128<kCachePolicyDevice>(
+            rpf, (uint32_t)((((QB * KS + s) * 64 + lane) * 8) * 2),
             make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
-                       pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
+                       pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3])));
       }
     }
     // ---- K K^T (the B operand, K rows of block KB, read once)
@@ -228,7 +230,7 @@ __global__ __launch_bounds__(256, HPW == 1 ? 8 : 4) void chunk_local_kernel(
   constexpr int NIB = F::NIB, KS = F::KS, AP = LL::AP;
   constexpr int NKI = C * D / 512;  // 1 KB pieces of the K (or Q) tile
   constexpr int KPR = D / 8;        // 16-byte pieces per row
-  static_assert(NIB == 1 || NIB == 2 || NIB == 4, "row sets");
+  static_assert(NIB == 1 || NIB == 2 || NIB == 4, "16-token blocks per chunk");
   __shared__ __attribute__((aligned(16))) LL L;
   uint16_t *Kt = L.u.kq;
 
@@ -350,9 +352,11 @@ __global__ __launch_bounds__(256, HPW == 1 ? 8 : 4) void chunk_local_kernel(
   // value head of the group writes them.
   if (gi == 0 && qrow && qfrag != nullptr) {  // one head set of the group
     const int64_t base = ((int64_t)cidx * hqk + hk) * (C * D);
-    uint16_t *qf = qfrag + base + ((int64_t)wave * F::DS * 64 + lane) * 8;
+    const rsrc_t rqf = make_rsrc(qfrag + base, C * D * 2);
 #pragma unroll
-    for (int s = 0; s < F::DS; ++s) *reinterpret_cast<uint4 *>(qf + s * 512) = qv[s];
+    for (int s = 0; s < F::DS; ++s)
+      buf_store_b128<kCachePolicyDevice>(rqf, (uint32_t)((((wave * F::DS + s) * 64 + lane) * 8) * 2),
+                                         qv[s]);
   }
 
   // ---- Gram tiles and decay masks: row `wave` of Q K^T, row NIB-1-wave of K K^T
@@ -453,15 +457,16 @@ __global__ __launch_bounds__(256, HPW == 1 ? 8 : 4) void chunk_local_kernel(
       Z[c][3] *= bc.w;
     }
     // T' as A-operand fragments, same token order as P.
-    uint16_t *tf = tfrag + slot * F::FRAG + ((int64_t)ib * KS * 64 + lane) * 8;
+    const rsrc_t rtf = make_rsrc(tfrag + slot * F::FRAG, F::FRAG * 2);
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       if (2 * s > ib) continue;  // above the diagonal: zero, never stored or read
       const f32x4 lo4 = Z[2 * s];
       const f32x4 hi4 = (2 * s + 1 < NIB) ? Z[(2 * s + 1) % NIB] : f32x4{0.f, 0.f, 0.f, 0.f};
-      *reinterpret_cast<uint4 *>(tf + s * 512) =
+      buf_store_b128<kCachePolicyDevice>(
+          rtf, (uint32_t)((((ib * KS + s) * 64 + lane) * 8) * 2),
           make_uint4(pack_bf16x2(lo4[0], lo4[1]), pack_bf16x2(lo4[2], lo4[3]),
-                     pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3]));
+                     pack_bf16x2(hi4[0], hi4[1]), pack_bf16x2(hi4[2], hi4[3])));
     }
   }
 }
