@@ -112,6 +112,73 @@ __device__ __forceinline__ int64_t seg_count(int64_t len, int64_t span) {
   return len <= span ? 1 : (len + span - 1) / span;
 }
 
+// ============================================================ dispatch order
+// The output launch runs one work-group per CU (its LDS), and work-groups
+// start in block order as CUs free up. In block order (sequence order) a long
+// sequence late in the batch starts late and finishes last: 16 sequences of
+// U[64, 8192] tokens with 32 value heads give a 175-step span of chunk steps
+// where the work is 122 steps per CU. Started longest first (list scheduling
+// with the longest jobs first), the same batch spans 130 steps.
+//
+// chain_order_kernel lists the segment slots in decreasing order of their
+// chunk count, for one work-group: a histogram over buckets of the count
+// (exact below 960 chunks, then one bucket per power of two), a scan, and a
+// scatter through per-bucket cursors (the order inside a bucket is whatever
+// the atomics give). Slots that no sequence owns follow as -1. Each slot is
+// still carried by exactly one set of work-groups, so the results do not
+// depend on the order.
+constexpr int kOrderThreads = 1024;
+constexpr int kOrderBuckets = kOrderThreads;
+
+// Bucket of a segment of `len` chunks, longest first.
+__device__ __forceinline__ int order_rank_bucket(int64_t len) {
+  const int b = len < 960 ? (int)len : 960 + (63 - __clzll((unsigned long long)len));
+  return kOrderBuckets - 1 - b;
+}
+
+__global__ __launch_bounds__(kOrderThreads) void chain_order_kernel(
+    const int32_t *__restrict__ cu, int n_seqs, int chunk, int seg_chunks, int64_t nseg,
+    int32_t *__restrict__ order) {
+  __shared__ int cursor[kOrderBuckets];
+  __shared__ int scan[kOrderBuckets];
+  const int tid = threadIdx.x;
+  const int64_t span = (int64_t)chunk * seg_chunks;
+  // Every segment s < G of sequence n: slot cu[n] / span + n + s, with
+  // min(nch, (s + 1) L) - s L chunks (the slot numbering of chain_kernel).
+  auto for_segments = [&](auto &&f) {
+    for (int n = tid; n < n_seqs; n += kOrderThreads) {
+      const int64_t a = cu[n], len = cu[n + 1] - a;
+      const int64_t G = seg_count(len, span), nch = (len + chunk - 1) / chunk;
+      const int64_t base = a / span + n;
+      for (int64_t sg = 0; sg < G; ++sg) {
+        const int64_t l = min(nch, (sg + 1) * seg_chunks) - sg * seg_chunks;
+        f(base + sg, order_rank_bucket(max(l, (int64_t)0)));
+      }
+    }
+  };
+  cursor[tid] = 0;
+  __syncthreads();
+  for_segments([&](int64_t, int rb) { atomicAdd(&cursor[rb], 1); });
+  __syncthreads();
+  const int own = cursor[tid];
+  scan[tid] = own;
+  __syncthreads();
+  for (int off = 1; off < kOrderBuckets; off <<= 1) {
+    const int add = tid >= off ? scan[tid - off] : 0;
+    __syncthreads();
+    scan[tid] += add;
+    __syncthreads();
+  }
+  cursor[tid] = scan[tid] - own;  // first rank of bucket tid
+  const int used = scan[kOrderBuckets - 1];
+  __syncthreads();
+  for_segments([&](int64_t slot, int rb) {
+    const int r = atomicAdd(&cursor[rb], 1);
+    if (r < nseg) order[r] = (int32_t)slot;  // (always, when cu[N] is the token count)
+  });
+  for (int64_t r = used + tid; r < nseg; r += kOrderThreads) order[r] = -1;
+}
+
 // Y operand of U = T' Y for token step st: Y = V - exp(gamma) X in the token
 // order of tok_pos, from the bf16 V operand (transpose reads of the V tile)
 // and the X accumulator tiles 2 st (slots 0-3) and 2 st + 1 (slots 4-7).
@@ -489,24 +556,27 @@ __global__ __launch_bounds__((ChainCfg<D, C, MAPS>::NT)) void chain_kernel(
     const int32_t *__restrict__ cu, const float *__restrict__ dec_ws,
     const uint16_t *__restrict__ tfrag, const uint16_t *__restrict__ pfrag, const float *s0,
     float *sT, __bf16 *__restrict__ o, float *__restrict__ bslot, uint16_t *__restrict__ mt_hi,
-    uint16_t *__restrict__ mt_lo, int n_seqs, int hqk, int hv, int group, int n_units,
-    int seg_chunks) {
+    uint16_t *__restrict__ mt_lo, const int32_t *__restrict__ order, int n_seqs, int hqk, int hv,
+    int group, int n_units, int seg_chunks) {
   using F = Cfg<D, C>;
   using H = ChainCfg<D, C, MAPS>;
   constexpr int NIB = F::NIB, KS = F::KS;
   constexpr bool OUT = !MAPS;
   __shared__ __attribute__((aligned(16))) ChainLds<D, C, MAPS> L;
 
-  // Block id -> (segment slot, key head) unit and head of the group. Work-
+  // Block id -> (segment rank, key head) unit and head of the group. Work-
   // groups are dealt to the eight XCDs round robin, so ids b and b + 8 share
   // one: the value heads of a group (which share K and Q) take ids
-  // 8 (group j + gi) + x.
+  // 8 (group j + gi) + x. The segment of rank r is order[r] (longest
+  // first; -1: no segment), or slot r when there is no order.
   const int bid = blockIdx.x;
   const int xg = bid & 7, jj = bid >> 3;
   const int gi = jj % group;
   const int unit = (jj / group) * 8 + xg;
   if (unit >= n_units) return;
-  const int slot = unit / hqk, hk = unit - slot * hqk;
+  const int rank = unit / hqk, hk = unit - rank * hqk;
+  const int slot = order != nullptr ? order[rank] : rank;
+  if (slot < 0) return;
   const int h = hk * group + gi;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
@@ -849,11 +919,21 @@ hipError_t launch_chain(const PrefillArgs &a, const PrefillWorkspace &ws) {
   const __bf16 *q = (const __bf16 *)a.q, *k = (const __bf16 *)a.k, *v = (const __bf16 *)a.v;
   __bf16 *o = (__bf16 *)a.o;
 
-  if (segmented) {
+  // Longest segments first in the output launch, when there is more than
+  // one sequence (the segments of one sequence are equal but for the last).
+  int32_t *order = nullptr;
+  if (a.n_seqs > 1) {
+    order = reinterpret_cast<int32_t *>(base + ws.order);
+    hipLaunchKernelGGL(chain_order_kernel, dim3(1), dim3(kOrderThreads), 0, a.stream,
+                       a.cu_seqlens, a.n_seqs, C, a.seg_chunks, nseg, order);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (segmented) {  // every map segment has L chunks: block order
     hipLaunchKernelGGL((chain_kernel<D, C, true>), dim3(bx), dim3(ChainCfg<D, C, true>::NT), 0,
                        a.stream, q, k, v, a.cu_seqlens, dec, tf, pf, a.initial_state,
-                       a.final_state, o, bs, mh, ml, a.n_seqs, a.hqk, a.hv, group, (int)units,
-                       a.seg_chunks);
+                       a.final_state, o, bs, mh, ml, nullptr, a.n_seqs, a.hqk, a.hv, group,
+                       (int)units, a.seg_chunks);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (ws.n_maps >= 2) {  // some sequence may have three or more segments
@@ -866,7 +946,8 @@ hipError_t launch_chain(const PrefillArgs &a, const PrefillWorkspace &ws) {
   }
   hipLaunchKernelGGL((chain_kernel<D, C, false>), dim3(bx), dim3(ChainCfg<D, C, false>::NT), 0,
                      a.stream, q, k, v, a.cu_seqlens, dec, tf, pf, a.initial_state, a.final_state,
-                     o, bs, mh, ml, a.n_seqs, a.hqk, a.hv, group, (int)units, a.seg_chunks);
+                     o, bs, mh, ml, order, a.n_seqs, a.hqk, a.hv, group, (int)units,
+                     a.seg_chunks);
   return hipGetLastError();
 }
 

@@ -57,6 +57,9 @@ struct PrefillWorkspace {
   size_t bslot;       // f32  [n_maps, HV, D, D]: B of a segment, then the composed state
   size_t mthi, mtlo;  // bf16 [n_maps, HV, D, D]: M^T of a segment, hi and lo parts
   int64_t n_maps;
+  // Whole-chain carry with more than one sequence: the segment slots, longest
+  // first (T / span + N int32).
+  size_t order;
   size_t total;
 };
 

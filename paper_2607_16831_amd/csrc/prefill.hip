@@ -733,6 +733,9 @@ PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
   p = align256(p + sizeof(uint16_t) * mbytes);
   w.mtlo = p;
   p = align256(p + sizeof(uint16_t) * mbytes);
+  w.order = p;
+  if (!wave && !tile && span > 0 && n_seqs > 1)  // (one sequence: block order)
+    p = align256(p + sizeof(int32_t) * (size_t)(n_tokens / span + n_seqs));
   w.total = p;
   return w;
 }

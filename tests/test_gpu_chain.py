@@ -116,3 +116,59 @@ def test_segments_gated():
     print("[chain] gated_L2 o=%.3e state=%.3e o_chain_max=%.3e state_chain_max=%.3e"
           % (e["o"], e["state"], e["o_max"], e["state_max"]), flush=True)
     assert e["o_max"] <= O_BAR and e["state_max"] <= STATE_BAR
+
+
+def _check_prefilled(name, x, dev, chunk):
+    """Outputs and final states start as NaN, so a segment that no work-group
+    carries (a hole in the longest-first order) cannot pass on stale memory."""
+    d = to_dev(x, dev)
+    T, hv, dv = d["v"].shape
+    n = len(x["cu_seqlens"]) - 1
+    o = torch.full((T, hv, dv), float("nan"), dtype=d["v"].dtype, device=dev)
+    fs = torch.full((n, hv, dv, d["k"].shape[2]), float("nan"), device=dev)
+    gdn.prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], d["cu_seqlens"],
+                initial_state=d["initial_state"], chunk=chunk, o=o, final_state=fs)
+    torch.cuda.synchronize()
+    o, sT = o.cpu(), fs.cpu()
+    o_ref, s_ref = oracle.prefill(x["q"], x["k"], x["v"], x["g"], x["beta"],
+                                  x["cu_seqlens"], x["initial_state"])
+    e = chain_errors(o, sT, o_ref, s_ref, x["cu_seqlens"].numpy())
+    print("[chain] %s o=%.3e state=%.3e o_chain_max=%.3e state_chain_max=%.3e worst=%s"
+          % (name, e["o"], e["state"], e["o_max"], e["state_max"], e["worst"]), flush=True)
+    assert torch.isfinite(o.float()).all() and torch.isfinite(sT).all()
+    assert e["o_max"] <= O_BAR and e["state_max"] <= STATE_BAR
+
+
+@pytest.mark.parametrize("seg", [64, 2])
+def test_longest_first_order_ragged(seg):
+    """More than one sequence: the output launch takes its segments longest
+    first from a list the library builds on the device. Lengths rising
+    through the batch (the order is reversed), an empty sequence; seg = 64
+    keeps every sequence in one segment, seg = 2 mixes two-chunk segments
+    with shorter last ones."""
+    dev = require_gpu()
+    lens = (0, 1, 70, 130, 300, 511, 777, 1000, 1500)
+    w = synth.PREFILL_4K.replace(seq_len=None, lengths=lens, n_seqs=len(lens), hqk=2, hv=4,
+                                 g_mu=-4.0, state_std=0.1, seed=313)
+    _check_prefilled("order_L%d" % seg, synth.make(w), dev, 64 | gdn.CHUNK_SEGMENT(seg))
+
+
+def test_longest_first_order_many_sequences():
+    """1100 sequences (more than the ordering work-group's 1024 threads), one
+    value head each: the whole-chain carry, every chain in the list once."""
+    dev = require_gpu()
+    rng = np.random.default_rng(317)
+    lens = tuple(int(v) for v in rng.integers(65, 200, size=1100))
+    w = synth.PREFILL_4K.replace(seq_len=None, lengths=lens, n_seqs=len(lens), hqk=1, hv=1, d=32,
+                                 g_mu=-4.0, state_std=0.1, seed=319)
+    _check_prefilled("order_many", synth.make(w), dev, 64)
+
+
+def test_longest_first_order_long_segments():
+    """Segments of more than 960 chunks (C = 16), which the order ranks by
+    power-of-two buckets, beside short ones."""
+    dev = require_gpu()
+    lens = (300, 15500, 40, 16000, 9000)
+    w = synth.PREFILL_4K.replace(seq_len=None, lengths=lens, n_seqs=len(lens), hqk=1, hv=1, d=32,
+                                 g_mu=-4.0, state_std=0.1, seed=321)
+    _check_prefilled("order_long_C16", synth.make(w), dev, 16 | gdn.CHUNK_SEGMENT(4095))
