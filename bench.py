@@ -338,7 +338,9 @@ def main():
     # The varlen batch (16 sequences, lengths U[64, 8192], nonzero initial
     # states) and the long-context pair (2 x 32768 tokens, strong decay), same
     # heads and d: time per call (events, 5 calls after 2 warm-up calls, one
-    # input set each), with the algorithmic flop count of the same formula.
+    # input set each) with 64-token chunks, with the algorithmic flop count of
+    # the same formula; then the same with the library's own chunk choice
+    # (chunk = 0; the varlen batch fixes no chunk size) when it differs.
     if not args.no_other_workloads:
         other = {}
         for w in (synth.PREFILL_VARLEN, synth.PREFILL_LONG):
@@ -347,27 +349,41 @@ def main():
             Tw = t["q"].shape[0]
             o = torch.empty((Tw, w.hv, w.d), dtype=torch.bfloat16, device=dev)
             fs = torch.empty((w.n_seqs, w.hv, w.d, w.d), device=dev)
-            ws = gdn.alloc_workspace(w.n_seqs, Tw, w.hqk, w.hv, w.d, w.chunk, dev)
+            ws = gdn.alloc_workspace(w.n_seqs, Tw, w.hqk, w.hv, w.d, gdn.CHUNK_AUTO, dev)
 
-            def call():
-                gdn.prefill(t["q"], t["k"], t["v"], t["g"], t["beta"], t["cu_seqlens"],
-                            initial_state=t["initial_state"], chunk=w.chunk, o=o,
-                            final_state=fs, workspace=ws)
-            for _ in range(2):
-                call()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(5):
-                call()
-            e1.record()
-            torch.cuda.synchronize()
-            us = e0.elapsed_time(e1) * 1e3 / 5
+            def time_chunk(chunk):
+                def call():
+                    gdn.prefill(t["q"], t["k"], t["v"], t["g"], t["beta"], t["cu_seqlens"],
+                                initial_state=t["initial_state"], chunk=chunk, o=o,
+                                final_state=fs, workspace=ws)
+                for _ in range(2):
+                    call()
+                torch.cuda.synchronize()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(5):
+                    call()
+                e1.record()
+                torch.cuda.synchronize()
+                return e0.elapsed_time(e1) * 1e3 / 5
+
+            us = time_chunk(w.chunk)
             fl = prefill_flops(Tw, w.hqk, w.hv, w.d, w.chunk)
-            other[w.name] = {"tokens": Tw, "us_per_call": round(us, 1),
-                             "tokens_per_s": round(Tw / (us * 1e-6), 1),
-                             "tflops": round(fl / (us * 1e-6) / 1e12, 2),
-                             "mfma_util": round(fl / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+            row = {"tokens": Tw, "chunk": w.chunk, "us_per_call": round(us, 1),
+                   "tokens_per_s": round(Tw / (us * 1e-6), 1),
+                   "tflops": round(fl / (us * 1e-6) / 1e12, 2),
+                   "mfma_util": round(fl / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+            ca = gdn.prefill_auto_chunk(w.n_seqs, Tw, w.hqk, w.hv, w.d, w.d)
+            row["auto_chunk"] = ca
+            if ca != w.chunk:
+                ua = time_chunk(gdn.CHUNK_AUTO)
+                fa = prefill_flops(Tw, w.hqk, w.hv, w.d, ca)
+                row.update({"us_per_call_auto": round(ua, 1),
+                            "tokens_per_s_auto": round(Tw / (ua * 1e-6), 1),
+                            "mfma_util_auto": round(fa / (ua * 1e-6) / 1e12 / PEAK_BF16_TFLOPS,
+                                                    4)})
+            other[w.name] = row
             del t, o, fs, ws
         out["prefill_other_workloads"] = other
 

@@ -83,6 +83,12 @@ struct ChainLds<D, C, false> {
   using F = Cfg<D, C>;
   using H = ChainCfg<D, C, false>;
   uint16_t K[H::NB][H::TILE];  // swizzled rows (kn_index); rows C..CP-1 stay zero
+  // 16 bytes between the K and Q tiles: at a distance of a multiple of 512
+  // bytes the compiler pairs each K-row read with the Q-row read of the same
+  // lane address into one two-address LDS read, whose results then need 64
+  // register copies per chunk to form the A operands; apart, each read lands
+  // in its operand's registers (66K-token batch: 1017 -> 974 us per call).
+  uint16_t kq_gap[8];
   uint16_t Q[H::NB][H::TILE];
   uint16_t V[H::NB][H::TILE];
   uint16_t T[H::NB][F::FRAG];  // T' as A-operand fragments (only those on or below the diagonal)

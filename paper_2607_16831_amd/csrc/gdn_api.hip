@@ -59,7 +59,14 @@ constexpr ChunkRule kChunkRules[] = {
     {128, 1, 4, 1536, 16, 320},
 };
 
-int32_t auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t d) {
+// Past those bounds, 64-token chunks unless both 64 and 32 would take the
+// whole-chain carry (many chains, or long ones): there 32-token chunks are
+// faster at every shape measured (d = 32, 64, 128; 16/32 heads; N x L from
+// 2 x 32768 to 256 x 256 tokens and the 16-sequence U[64, 8192] batch): by
+// 6-20%, e.g. 16 x 4096 tokens at d = 128 858 against 941 us, 2 x 32768 1293
+// against 1370 us. With the per-tile carry (few short chains: 1 x 8192
+// tokens, 144 against 224 us) 64 stays.
+int32_t auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hv, int32_t d) {
   if (n_seqs <= 0) return 64;
   ChunkRule r = kChunkRules[2];
   for (const ChunkRule &c : kChunkRules)
@@ -68,7 +75,11 @@ int32_t auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t d) {
   if (avg <= r.serial || (avg <= r.serial_big && n_seqs >= r.n_big)) return 1;
   if (avg <= r.c16) return 16;
   if (avg <= r.c32) return 32;
-  return 64;
+  auto whole_chain = [&](int c) {
+    return !gdn::uses_wave_carry(n_seqs, n_tokens, c) &&
+           !gdn::uses_tile_carry(n_seqs, n_tokens, hv, c);
+  };
+  return (whole_chain(64) && whole_chain(32)) ? 32 : 64;
 }
 
 // The `chunk` argument: a size (0, 1, 16, 32, 64), optionally OR-ed with
@@ -163,7 +174,7 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
   if (!ca.ok) return GDN_ERR_UNSUPPORTED;
   const bool neumann = ca.neumann;
   chunk = ca.size;
-  if (chunk == 0 && !neumann) chunk = auto_chunk(n_seqs, n_tokens, dk);
+  if (chunk == 0 && !neumann) chunk = auto_chunk(n_seqs, n_tokens, hv, dk);
   if (!supported_head(dk, dv) || !supported_chunk(chunk) || !supported_dtype(dtype) ||
       (neumann && chunk < 16) || ((ca.seg > 0 || ca.tiles) && ca.size == 1))
     return GDN_ERR_UNSUPPORTED;
@@ -279,7 +290,7 @@ int32_t gdn_prefill_auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hqk, in
                                int32_t dk, int32_t dv) {
   if (n_seqs < 0 || n_tokens < 0 || n_tokens > INT32_MAX) return 0;
   if (check_heads(hqk, hv) != GDN_OK || !supported_head(dk, dv)) return 0;
-  return auto_chunk(n_seqs, n_tokens, dk);
+  return auto_chunk(n_seqs, n_tokens, hv, dk);
 }
 
 gdn_status gdn_prefill(const void *q, const void *k, const void *v,

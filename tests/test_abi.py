@@ -89,17 +89,22 @@ def test_auto_chunk_rule():
     ac = gdn.prefill_auto_chunk
     picks = [ac(n, t, 16, 32, 128, 128) for n, t in
              ((4096, 4096), (512, 2048), (128, 128 * 12), (64, 64 * 40), (1, 4096),
-              (16, 66000))]
-    # measured choices at d = 128: token-serial for single tokens, then 16, 32, 64
-    assert picks == [1, 16, 16, 32, 64, 64]
+              (1, 8192), (16, 66000), (2, 65536))]
+    # measured choices at d = 128: token-serial for single tokens, then 16, 32,
+    # 64 while the per-tile carry runs (few, short chains), 32 where both 64
+    # and 32 take the whole-chain carry (many chains, or long ones)
+    assert picks == [1, 16, 16, 32, 64, 64, 32, 32]
     # many sequences of a few tokens: token-serial at d = 128
     assert ac(2048, 8192, 16, 32, 128, 128) == 1 and ac(512, 2048, 16, 32, 128, 128) == 16
     order = {1: 0, 16: 1, 32: 2, 64: 3}
     for d in (32, 64, 128):
-        # every length maps to a built size, monotone in the average length
+        # every length maps to a built size, monotone in the average length up
+        # to where 64 sequences x 32 heads take the whole-chain carry at 32-
+        # and 64-token chunks (L > 64), which runs 32-token chunks
         avg = [ac(64, 64 * L, 16, 32, d, d) for L in range(1, 1200)]
-        assert set(avg) <= {1, 16, 32, 64} and avg[0] == 1 and avg[-1] == 64
-        assert all(order[a] <= order[b] for a, b in zip(avg, avg[1:]))
+        assert set(avg) <= {1, 16, 32, 64} and avg[0] == 1 and avg[-1] == 32
+        assert all(order[a] <= order[b] for a, b in zip(avg[:64], avg[1:64]))
+        assert set(avg[64:]) == {32}
         # the average is rounded up: 64 sequences of 8 and one of 9 tokens
         # count as 9
         assert ac(65, 64 * 8 + 9, 16, 32, d, d) == ac(1, 9, 16, 32, d, d)
