@@ -62,8 +62,12 @@ struct ChainCfg {
   static constexpr int NWR = D / (16 * NJ);     // compute wavefronts per set of D rows
   static constexpr int NCW = MAPS ? 2 * NWR : NWR;  // compute wavefronts
   static constexpr int NT = 64 * (NCW + 2);     // threads: compute, a loader and a prefetcher
-  static constexpr int TILE = F::CP * D;        // bf16 elements of a K / Q / V tile
-  static constexpr int NKI = C * D / 512;       // 1 KB copies of a K / Q / V chunk
+  // K, Q and V tiles: rows of P = D + 8 bf16 (see chain_tile_copy_offset),
+  // CP rows (those past C stay zero), and room for the last 1 KB copy.
+  static constexpr int P = D + 8;               // row pitch, elements
+  static constexpr int PPR = D / 8 + 1;         // 16-byte pieces per row, the last one padding
+  static constexpr int NKI = (C * PPR + 63) / 64;  // 1 KB copies of a K / Q / V chunk
+  static constexpr int TILE = NKI * 512 > F::CP * P ? NKI * 512 : F::CP * P;  // elements
   static constexpr int NB = 2;                  // LDS buffers (chunk i uses buffer i % 2)
   // L2 prefetch of the chunk PFD ahead of the one in use: one 128-byte line
   // per lane and load, over the K, Q and V rows and the T', P and decay
@@ -82,7 +86,7 @@ template <int D, int C>
 struct ChainLds<D, C, false> {
   using F = Cfg<D, C>;
   using H = ChainCfg<D, C, false>;
-  uint16_t K[H::NB][H::TILE];  // swizzled rows (kn_index); rows C..CP-1 stay zero
+  uint16_t K[H::NB][H::TILE];  // rows at pitch P; rows C..CP-1 stay zero
   // 16 bytes between the K and Q tiles: at a distance of a multiple of 512
   // bytes the compiler pairs each K-row read with the Q-row read of the same
   // lane address into one two-address LDS read, whose results then need 64
@@ -116,6 +120,52 @@ struct ChainLds<D, C, true> {
 // (disjoint; below T / span, since G_n - 1 <= floor(len_n / span)).
 __device__ __forceinline__ int64_t seg_count(int64_t len, int64_t span) {
   return len <= span ? 1 : (len + span - 1) / span;
+}
+
+// ============================================================ chunk tiles
+// The K, Q and V tiles of a chunk sit in LDS row by row at a pitch of D + 8
+// bf16 (16 bytes of padding per row). The pitch in 16-byte units, D/8 + 1,
+// is odd, so the 16 rows of a matrix-operand read (one 16-byte piece per
+// row) fall on 16 distinct groups of four banks, as an XOR swizzle would
+// arrange; unlike a swizzle, the address of every operand read of a chunk is
+// one lane base plus a constant, which the compiler folds into the
+// instruction's offset instead of forming an address per read.
+//
+// The tiles are filled by buffer-to-LDS copies, 16 bytes per lane, lane i of
+// copy m landing at piece 64 m + i: the source offset of a piece is that of
+// its row and column, and padding pieces (and pieces past the chunk's C
+// rows) read out of range, as zeros.
+template <int D, int C>
+__device__ __forceinline__ uint32_t chain_tile_copy_offset(int m, int lane, int stride) {
+  constexpr int PPR = D / 8 + 1;
+  const int p = 64 * m + lane, row = p / PPR, pc = p - row * PPR;
+  return (pc < D / 8 && row < C) ? (uint32_t)((row * stride + 8 * pc) * 2) : kOutOfRange;
+}
+
+// Element index of (row, column) in a tile.
+template <int D>
+__device__ __forceinline__ int ptile_index(int row, int col) {
+  return row * (D + 8) + col;
+}
+
+// Rows of a tile as the transposed operand of a contraction over its rows
+// (K^T for the state update, V for Y): lane (l16, g4) gets T[j][16 t + l16]
+// for the 8 rows at positions 32 s + 8 g4 + [0, 8), in the token order of
+// tok_pos. Each transpose load serves 4 rows: lanes 4m..4m+3 of a 16-lane
+// group point at row j_m, columns 16 t + 4 (l16 % 4) + [0, 4).
+template <int D>
+__device__ __forceinline__ uint4 ptile_t_operand(const uint16_t *T, int t, int s, int l16, int g4) {
+  uint32_t w[4];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int j = 32 * s + 16 * hh + 4 * g4 + (l16 >> 2);
+    const uint16_t *p = T + ptile_index<D>(j, 16 * t + 4 * (l16 & 3));
+    const v4i16 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_v4i16 *)(const_cast<uint16_t *>(p)));
+    w[2 * hh] = (uint32_t)(uint16_t)x[0] | ((uint32_t)(uint16_t)x[1] << 16);
+    w[2 * hh + 1] = (uint32_t)(uint16_t)x[2] | ((uint32_t)(uint16_t)x[3] << 16);
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 // ============================================================ dispatch order
@@ -288,8 +338,8 @@ __device__ __forceinline__ void chain_compute(Lds &L, int wave, int lane, const 
 #pragma unroll
       for (int st = 0; st < DS; ++st) {
         const int row = 16 * ib + l16, col = 32 * st + 4 * g4;
-        a[st] = key_operand(*reinterpret_cast<const uint2 *>(&Tl[kn_index<D>(row, col)]),
-                            *reinterpret_cast<const uint2 *>(&Tl[kn_index<D>(row, col + 16)]));
+        a[st] = key_operand(*reinterpret_cast<const uint2 *>(&Tl[ptile_index<D>(row, col)]),
+                            *reinterpret_cast<const uint2 *>(&Tl[ptile_index<D>(row, col + 16)]));
       }
     };
     auto frag = [&](const uint16_t *Fl, int ib, int st) {
@@ -306,7 +356,7 @@ __device__ __forceinline__ void chain_compute(Lds &L, int wave, int lane, const 
       for (int j = 0; j < NJ; ++j) {
 #pragma unroll
         for (int st = 0; st < KS; ++st)
-          vb[j][st] = USE_V ? kt_operand<D>(Vt, v0 / 16 + j, st, l16, g4) : make_uint4(0, 0, 0, 0);
+          vb[j][st] = USE_V ? ptile_t_operand<D>(Vt, v0 / 16 + j, st, l16, g4) : make_uint4(0, 0, 0, 0);
       }
     };
     if constexpr (OUT) {
@@ -367,8 +417,8 @@ __device__ __forceinline__ void chain_compute(Lds &L, int wave, int lane, const 
       auto krd = [&](int n) {
         const int st = n / NIB, ib = n % NIB;
         const int row = 16 * ib + l16, col = 32 * st + 4 * g4;
-        return key_operand(*reinterpret_cast<const uint2 *>(&Kt[kn_index<D>(row, col)]),
-                           *reinterpret_cast<const uint2 *>(&Kt[kn_index<D>(row, col + 16)]));
+        return key_operand(*reinterpret_cast<const uint2 *>(&Kt[ptile_index<D>(row, col)]),
+                           *reinterpret_cast<const uint2 *>(&Kt[ptile_index<D>(row, col + 16)]));
       };
       uint4 kr[NS];
 #pragma unroll
@@ -431,8 +481,8 @@ __device__ __forceinline__ void chain_compute(Lds &L, int wave, int lane, const 
     auto read_kt01 = [&]() {
 #pragma unroll
       for (int st = 0; st < KS; ++st) {
-        kt0[st] = kt_operand<D>(Kt, 0, st, l16, g4);
-        kt1[st] = kt_operand<D>(Kt, NKT > 1 ? 1 : 0, st, l16, g4);
+        kt0[st] = ptile_t_operand<D>(Kt, 0, st, l16, g4);
+        kt1[st] = ptile_t_operand<D>(Kt, NKT > 1 ? 1 : 0, st, l16, g4);
       }
     };
     if constexpr (OUT) read_kt01();  // (the map launch reads them after U: registers)
@@ -502,7 +552,7 @@ __device__ __forceinline__ void chain_compute(Lds &L, int wave, int lane, const 
         __builtin_amdgcn_sched_barrier(0);
         if (t + 2 < NKT) {
 #pragma unroll
-          for (int st = 0; st < KS; ++st) kn[st] = kt_operand<D>(Kt, t + 2, st, l16, g4);
+          for (int st = 0; st < KS; ++st) kn[st] = ptile_t_operand<D>(Kt, t + 2, st, l16, g4);
         }
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
@@ -625,7 +675,7 @@ __global__ __launch_bounds__((ChainCfg<D, C, MAPS>::NT)) void chain_kernel(
 
   // token rows C..CP-1 of the K and V tiles stay zero (transpose reads cover CP rows)
   if (C < F::CP) {
-    for (int idx = C * D + tid; idx < F::CP * D; idx += H::NT) {
+    for (int idx = C * H::P + tid; idx < F::CP * H::P; idx += H::NT) {
 #pragma unroll
       for (int bb = 0; bb < H::NB; ++bb) {
         L.K[bb][idx] = 0;
@@ -644,19 +694,19 @@ __global__ __launch_bounds__((ChainCfg<D, C, MAPS>::NT)) void chain_kernel(
       const rsrc_t rv = make_rsrc(v + (t0 * hv + h) * D, (uint32_t)(nv * vstride * 2));
 #pragma unroll
       for (int m = 0; m < H::NKI; ++m) {
-        const uint32_t off = tile_copy_offset<D>(m, lane, kstride);
+        const uint32_t off = chain_tile_copy_offset<D, C>(m, lane, kstride);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void *)&L.K[bb][512 * m], 16, off, 0, 0, 0);
       }
 #pragma unroll
       for (int m = 0; m < H::NKI; ++m) {
-        const uint32_t off = tile_copy_offset<D>(m, lane, vstride);
+        const uint32_t off = chain_tile_copy_offset<D, C>(m, lane, vstride);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void *)&L.V[bb][512 * m], 16, off, 0, 0, 0);
       }
       if constexpr (OUT) {
         const rsrc_t rq = make_rsrc(q + (t0 * hqk + hk) * D, (uint32_t)(nv * kstride * 2));
 #pragma unroll
         for (int m = 0; m < H::NKI; ++m) {
-          const uint32_t off = tile_copy_offset<D>(m, lane, kstride);
+          const uint32_t off = chain_tile_copy_offset<D, C>(m, lane, kstride);
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_void *)&L.Q[bb][512 * m], 16, off, 0, 0, 0);
         }
       }
