@@ -130,7 +130,9 @@ size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
  * the average sequence length T_total / N (rounded up) and N, with bounds
  * measured on MI355X. Very short sequences take the token-serial path, where
  * the chunked form's per-chunk work does not pay; longer ones take 16, 32 or
- * 64 as the average length grows. Pure host function; no HIP call.
+ * 64 as the average length grows, except that batches with many or long
+ * chains, which take the whole-chain carry at both 32 and 64, take 32.
+ * Pure host function; no HIP call.
  */
 int32_t gdn_prefill_auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hqk,
                                int32_t hv, int32_t dk, int32_t dv);
