@@ -504,11 +504,16 @@ __global__ __launch_bounds__(kCarryThreads) void chunk_carry_kernel(
         *reinterpret_cast<uint2 *>(&L.Sl[s_slot(wave, l16, g4)]) =
             pack4_bf16(S[0], S[1], S[2], S[3]);
       lds_barrier();
-      if (wave < 4)
+      if (wave < 4) {
+        // The X -> Y -> U chain is the critical path of every chunk: its
+        // wavefronts issue first when they compete with the output ones on
+        // a SIMD (4096 tokens: 77.6 -> 77.1 us per call, 16 calls each).
+        __builtin_amdgcn_s_setprio(1);
         carry_compute_xu<D, C, TIn>(L, S, wave, lane, nch, c0, tfrag, h, hv);
-      else
+      } else {
         carry_compute_o<D, C, TIn>(L, S, wave, lane, nch, c0, pfrag, qfrag, o, seq_t0, seq_t1,
                                    h, hk, hqk, hv, v0);
+      }
     } else {
       const uint16_t *ksrc = reinterpret_cast<const uint16_t *>(k);
       const int kstride = hqk * D;
