@@ -184,7 +184,7 @@ __device__ __forceinline__ uint4 ptile_t_operand(const uint16_t *T, int t, int s
 // still carried by exactly one set of work-groups, so the results do not
 // depend on the order.
 constexpr int kOrderThreads = 1024;
-constexpr int kOrderBuckets = kOrderThreads;
+constexpr int kOrderBuckets = 1024;
 
 // Bucket of a segment of `len` chunks, longest first.
 __device__ __forceinline__ int order_rank_bucket(int64_t len) {
@@ -192,17 +192,19 @@ __device__ __forceinline__ int order_rank_bucket(int64_t len) {
   return kOrderBuckets - 1 - b;
 }
 
-__global__ __launch_bounds__(kOrderThreads) void chain_order_kernel(
-    const int32_t *__restrict__ cu, int n_seqs, int chunk, int seg_chunks, int64_t nseg,
-    int32_t *__restrict__ order) {
-  __shared__ int cursor[kOrderBuckets];
-  __shared__ int scan[kOrderBuckets];
+// Builds the list in one work-group of NTH threads. cursor (kOrderBuckets
+// ints) and part (NTH ints) are LDS arrays of the caller.
+template <int NTH>
+__device__ void build_order(const int32_t *__restrict__ cu, int n_seqs, int chunk, int seg_chunks,
+                            int64_t nseg, int32_t *__restrict__ order, int *cursor, int *part) {
+  static_assert(kOrderBuckets % NTH == 0, "whole buckets per thread");
+  constexpr int BPT = kOrderBuckets / NTH;  // consecutive buckets per thread in the scan
   const int tid = threadIdx.x;
   const int64_t span = (int64_t)chunk * seg_chunks;
   // Every segment s < G of sequence n: slot cu[n] / span + n + s, with
   // min(nch, (s + 1) L) - s L chunks (the slot numbering of chain_kernel).
   auto for_segments = [&](auto &&f) {
-    for (int n = tid; n < n_seqs; n += kOrderThreads) {
+    for (int n = tid; n < n_seqs; n += NTH) {
       const int64_t a = cu[n], len = cu[n + 1] - a;
       const int64_t G = seg_count(len, span), nch = (len + chunk - 1) / chunk;
       const int64_t base = a / span + n;
@@ -212,27 +214,46 @@ __global__ __launch_bounds__(kOrderThreads) void chain_order_kernel(
       }
     }
   };
-  cursor[tid] = 0;
+  for (int b = tid; b < kOrderBuckets; b += NTH) cursor[b] = 0;
   __syncthreads();
   for_segments([&](int64_t, int rb) { atomicAdd(&cursor[rb], 1); });
   __syncthreads();
-  const int own = cursor[tid];
-  scan[tid] = own;
+  int loc[BPT], sum = 0;
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    loc[i] = cursor[BPT * tid + i];
+    sum += loc[i];
+  }
+  part[tid] = sum;
   __syncthreads();
-  for (int off = 1; off < kOrderBuckets; off <<= 1) {
-    const int add = tid >= off ? scan[tid - off] : 0;
+  for (int off = 1; off < NTH; off <<= 1) {  // inclusive scan of the per-thread sums
+    const int add = tid >= off ? part[tid - off] : 0;
     __syncthreads();
-    scan[tid] += add;
+    part[tid] += add;
     __syncthreads();
   }
-  cursor[tid] = scan[tid] - own;  // first rank of bucket tid
-  const int used = scan[kOrderBuckets - 1];
+  int run = part[tid] - sum;  // first rank of bucket BPT * tid
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    cursor[BPT * tid + i] = run;
+    run += loc[i];
+  }
+  const int used = part[NTH - 1];
   __syncthreads();
   for_segments([&](int64_t slot, int rb) {
     const int r = atomicAdd(&cursor[rb], 1);
     if (r < nseg) order[r] = (int32_t)slot;  // (always, when cu[N] is the token count)
   });
-  for (int64_t r = used + tid; r < nseg; r += kOrderThreads) order[r] = -1;
+  for (int64_t r = used + tid; r < nseg; r += NTH) order[r] = -1;
+}
+
+// The list on its own, when no composition launch runs to carry it.
+__global__ __launch_bounds__(kOrderThreads) void chain_order_kernel(
+    const int32_t *__restrict__ cu, int n_seqs, int chunk, int seg_chunks, int64_t nseg,
+    int32_t *__restrict__ order) {
+  __shared__ int cursor[kOrderBuckets];
+  __shared__ int part[kOrderThreads];
+  build_order<kOrderThreads>(cu, n_seqs, chunk, seg_chunks, nseg, order, cursor, part);
 }
 
 // Y operand of U = T' Y for token step st: Y = V - exp(gamma) X in the token
@@ -852,12 +873,27 @@ struct ComposeCfg {
 template <int D>
 __global__ __launch_bounds__(64 * ComposeCfg<D>::NW) void compose_kernel(
     const int32_t *__restrict__ cu, float *__restrict__ bslot, const uint16_t *__restrict__ mt_hi,
-    const uint16_t *__restrict__ mt_lo, int hv, int64_t span) {
+    const uint16_t *__restrict__ mt_lo, int hv, int64_t span, int n_seqs, int chunk,
+    int seg_chunks, int64_t nseg, int32_t *__restrict__ order) {
   using CC = ComposeCfg<D>;
   constexpr int NKT = CC::NKT, KTW = CC::KTW, DS = CC::DS, NVT = D / 16;
-  __shared__ __attribute__((aligned(16))) float xch[NKT][64 * 4];
+  constexpr int NTH = 64 * CC::NW;
+  __shared__ __attribute__((aligned(16))) union {
+    float xch[NKT][64 * 4];
+    struct {
+      int cursor[kOrderBuckets];
+      int part[NTH];
+    } ord;
+  } sh;
+  auto &xch = sh.xch;
 
   const int bid = blockIdx.x;
+  // With `order`, one work-group past the compositions builds the output
+  // launch's longest-first list (a launch saved; nothing here reads it).
+  if (order != nullptr && bid == (int)gridDim.x - 1) {
+    build_order<NTH>(cu, n_seqs, chunk, seg_chunks, nseg, order, sh.ord.cursor, sh.ord.part);
+    return;
+  }
   const int vt = bid % NVT, ph = bid / NVT;
   const int h = ph % hv, n = ph / hv;
   const int64_t a0 = cu[n], a1 = cu[n + 1];
@@ -976,10 +1012,12 @@ hipError_t launch_chain(const PrefillArgs &a, const PrefillWorkspace &ws) {
   __bf16 *o = (__bf16 *)a.o;
 
   // Longest segments first in the output launch, when there is more than
-  // one sequence (the segments of one sequence are equal but for the last).
-  int32_t *order = nullptr;
-  if (a.n_seqs > 1) {
-    order = reinterpret_cast<int32_t *>(base + ws.order);
+  // one sequence (the segments of one sequence are equal but for the last):
+  // built by an extra work-group of the composition launch when that runs,
+  // else by a launch of its own.
+  int32_t *order = a.n_seqs > 1 ? reinterpret_cast<int32_t *>(base + ws.order) : nullptr;
+  const bool compose = segmented && ws.n_maps >= 2;  // some sequence may have 3+ segments
+  if (order != nullptr && !compose) {
     hipLaunchKernelGGL(chain_order_kernel, dim3(1), dim3(kOrderThreads), 0, a.stream,
                        a.cu_seqlens, a.n_seqs, C, a.seg_chunks, nseg, order);
     const hipError_t e = hipGetLastError();
@@ -992,10 +1030,11 @@ hipError_t launch_chain(const PrefillArgs &a, const PrefillWorkspace &ws) {
                        (int)units, a.seg_chunks);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (ws.n_maps >= 2) {  // some sequence may have three or more segments
-      hipLaunchKernelGGL((compose_kernel<D>), dim3((unsigned)(a.n_seqs * a.hv * (D / 16))),
+    if (compose) {
+      const int64_t cblocks = (int64_t)a.n_seqs * a.hv * (D / 16) + (order != nullptr ? 1 : 0);
+      hipLaunchKernelGGL((compose_kernel<D>), dim3((unsigned)cblocks),
                          dim3(64 * ComposeCfg<D>::NW), 0, a.stream, a.cu_seqlens, bs, mh, ml,
-                         a.hv, span);
+                         a.hv, span, a.n_seqs, C, a.seg_chunks, nseg, order);
       e = hipGetLastError();
       if (e != hipSuccess) return e;
     }

@@ -58,7 +58,7 @@ def test_segments_ragged(chunk, seg, g_mu):
 
 
 @pytest.mark.parametrize("d", [32, 64])
-@pytest.mark.parametrize("chunk", [16, 64])
+@pytest.mark.parametrize("chunk", [16, 32, 64])
 def test_segments_head_sizes(d, chunk):
     dev = require_gpu()
     w = synth.PREFILL_4K.replace(seq_len=None, lengths=LENS, n_seqs=len(LENS), hqk=2, hv=4, d=d,

@@ -252,7 +252,8 @@ def test_serial_gated_launch_paths(n_seqs, lengths):
 
 
 # ------------------------------------------------------------ chunk = 0
-@pytest.mark.parametrize("n_seqs,length", [(256, 1), (256, 3), (64, 12), (48, 40), (8, 200), (2, 400)])
+@pytest.mark.parametrize("n_seqs,length", [(256, 1), (256, 3), (64, 12), (48, 40), (8, 200), (2, 400),
+                                           (16, 512)])
 def test_auto_runs_the_reported_path(n_seqs, length):
     """chunk = 0 at the benchmark's heads: bitwise the path the library
     reports, and within that path's oracle bars."""
