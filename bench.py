@@ -19,9 +19,12 @@ fixed algorithmic counts:
   decode bytes  = 2 B HV d^2 4 + B (2 HQK + 2 HV) d 2 + 8 B HV
 `traffic` is the counter-measured byte count per launch (see MEASURED_TRAFFIC).
 
-Alongside: `decode_latency_us` (one decode step per batch size, graph-replayed)
-and `prefill_dispatch` (short-sequence batches: the library's chunk choice
-against the fixed 64-token chunk).
+Alongside: the per-call spread (`us_per_call_dist`, `us_per_step_dist`: p10,
+p50, p90 over 100 calls, each between its own events), `decode_latency_us`
+(one decode step per batch size, graph-replayed), `prefill_dispatch`
+(short-sequence batches: the library's chunk choice against the fixed 64-token
+chunk) and `prefill_other_workloads` (the 66K-token varlen batch and the
+2 x 32768-token prefill).
 """
 import argparse
 import glob
@@ -203,6 +206,22 @@ def main():
     pre_cold_avg = ec[0].elapsed_time(ec[1]) / 1e3 / K
     del wss
 
+    # Per-call spread: 100 prefill calls, then 100 decode steps, each between
+    # a pair of events of its own (rotating input sets, shared workspace).
+    def per_call(fn, items, n=100):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n)]
+        for i in range(n):
+            evs[i][0].record()
+            fn(items[i % len(items)])
+            evs[i][1].record()
+        torch.cuda.synchronize()
+        ts = sorted(a.elapsed_time(b) * 1e3 for a, b in evs)
+        return {"calls": n, "p10": round(ts[n // 10], 2), "p50": round(ts[n // 2], 2),
+                "p90": round(ts[(9 * n) // 10], 2)}
+    pre_dist = per_call(run_prefill, P)
+    dec_dist = per_call(run_decode, D)
+
     pre_s = ev[0].elapsed_time(ev[1]) / 1e3
     dec_s = ev[1].elapsed_time(ev[2]) / 1e3
     T = P[0]["q"].shape[0]
@@ -245,9 +264,11 @@ def main():
         "prefill": {"us_per_call": round(pre_avg * 1e6, 2),
                     "us_per_call_workspace_per_set": round(pre_cold_avg * 1e6, 2),
                     "tokens_per_s": round(pre_tps, 1), "tflops": round(pre_tflops, 2),
-                    "mfma_util": round(pre_tflops / PEAK_BF16_TFLOPS, 4)},
+                    "mfma_util": round(pre_tflops / PEAK_BF16_TFLOPS, 4),
+                    "us_per_call_dist": pre_dist},
         "decode": {"us_per_step": round(dec_avg * 1e6, 2),
-                   "hbm_gbs": round(dec_gbs, 1), "hbm_frac": round(dec_gbs / PEAK_HBM_GBS, 4)},
+                   "hbm_gbs": round(dec_gbs, 1), "hbm_frac": round(dec_gbs / PEAK_HBM_GBS, 4),
+                   "us_per_step_dist": dec_dist},
         "roofline": dominant,
         "rooflines": [roof_pre, roof_dec],
     }
