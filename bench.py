@@ -48,8 +48,8 @@ METRIC = "prefill tokens/sec + MFMA util; decode µs/step + achieved HBM GB/s"
 # the kernel sources they were taken on. Any change to those sources makes
 # the figures stale, and `traffic` is then reported as null.
 MEASURED_TRAFFIC = {
-    "fdcab9032d08eca62fa354e693f15a80621e81799a51fa83a5f799d9dcf8e878":
-        {"prefill": 224048186, "decode": 274400153},
+    "a4b6d8185ad1db431f8f77488d3db51b12a672843d2bb1e624780d6f3db7e947":
+        {"prefill": 223783917, "decode": 274395415},
 }
 
 
