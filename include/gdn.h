@@ -131,7 +131,8 @@ size_t gdn_prefill_workspace_size(int32_t n_seqs, int64_t n_tokens,
  * measured on MI355X. Very short sequences take the token-serial path, where
  * the chunked form's per-chunk work does not pay; longer ones take 16, 32 or
  * 64 as the average length grows, except that batches with many or long
- * chains, which take the whole-chain carry at both 32 and 64, take 32.
+ * chains, which take the whole-chain carry at 32 (at d = 32: at 32 and 64),
+ * take 32.
  * Pure host function; no HIP call.
  */
 int32_t gdn_prefill_auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hqk,

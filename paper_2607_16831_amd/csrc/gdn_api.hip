@@ -59,13 +59,16 @@ constexpr ChunkRule kChunkRules[] = {
     {128, 1, 4, 1536, 16, 320},
 };
 
-// Past those bounds, 64-token chunks unless both 64 and 32 would take the
-// whole-chain carry (many chains, or long ones): there 32-token chunks are
-// faster at every shape measured (d = 32, 64, 128; 16/32 heads; N x L from
-// 2 x 32768 to 256 x 256 tokens and the 16-sequence U[64, 8192] batch): by
-// 6-20%, e.g. 16 x 4096 tokens at d = 128 858 against 941 us, 2 x 32768 1293
-// against 1370 us. With the per-tile carry (few short chains: 1 x 8192
-// tokens, 144 against 224 us) 64 stays.
+// Past those bounds, 64-token chunks unless 32 would take the whole-chain
+// carry (many chains, or long ones) -- at d = 32 only if 64 would take it
+// too. Measured (16/32 heads): where both take it, 32 is 6-20% faster at
+// every d (16 x 4096 tokens at d = 128: 858 against 941 us; 2 x 32768: 1293
+// against 1370 us); where 64 would take the per-tile carry instead, 32 is
+// 7-41% faster at d = 64 and 128 (4 x 4096 tokens: 263 against 377 us;
+// 1 x 16384 at d = 64: 148 against 251 us) but slower at d = 32 (4 x 4096:
+// 127 against 95 us, two tiles per chain there). Where 32 takes the per-tile
+// carry too (1 x 8192 tokens: 144 against 224 us; 3 x 4096: 252 against
+// 322 us), 64 stays.
 int32_t auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hv, int32_t d) {
   if (n_seqs <= 0) return 64;
   ChunkRule r = kChunkRules[2];
@@ -79,7 +82,7 @@ int32_t auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hv, int32_t d) {
     return !gdn::uses_wave_carry(n_seqs, n_tokens, c) &&
            !gdn::uses_tile_carry(n_seqs, n_tokens, hv, c);
   };
-  return (whole_chain(64) && whole_chain(32)) ? 32 : 64;
+  return (whole_chain(32) && (d >= 64 || whole_chain(64))) ? 32 : 64;
 }
 
 // The `chunk` argument: a size (0, 1, 16, 32, 64), optionally OR-ed with

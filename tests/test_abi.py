@@ -89,11 +89,14 @@ def test_auto_chunk_rule():
     ac = gdn.prefill_auto_chunk
     picks = [ac(n, t, 16, 32, 128, 128) for n, t in
              ((4096, 4096), (512, 2048), (128, 128 * 12), (64, 64 * 40), (1, 4096),
-              (1, 8192), (16, 66000), (2, 65536))]
+              (1, 8192), (3, 12288), (16, 66000), (2, 65536), (4, 16384), (1, 16384))]
     # measured choices at d = 128: token-serial for single tokens, then 16, 32,
-    # 64 while the per-tile carry runs (few, short chains), 32 where both 64
-    # and 32 take the whole-chain carry (many chains, or long ones)
-    assert picks == [1, 16, 16, 32, 64, 64, 32, 32]
+    # 64 while 32 would take the per-tile carry (few, short chains), 32 where
+    # 32 takes the whole-chain carry (many chains, or long ones)
+    assert picks == [1, 16, 16, 32, 64, 64, 64, 32, 32, 32, 32]
+    # at d = 32 only where 64 takes the whole-chain carry too
+    assert ac(4, 16384, 16, 32, 32, 32) == 64 and ac(4, 16384, 16, 32, 64, 64) == 32
+    assert ac(16, 66000, 16, 32, 32, 32) == 32
     # many sequences of a few tokens: token-serial at d = 128
     assert ac(2048, 8192, 16, 32, 128, 128) == 1 and ac(512, 2048, 16, 32, 128, 128) == 16
     order = {1: 0, 16: 1, 32: 2, 64: 3}
@@ -337,7 +340,10 @@ def test_scratch_prefill_validation():
     assert gdn.prefill_workspace_size(1, 16384, 16, 32, 128, 128, 64) > \
         gdn.PREFILL_SCRATCH_MAX_BYTES
     assert call(**big) == E.GDN_ERR_WORKSPACE
-    assert call(**dict(big, chunk=0)) == E.GDN_ERR_WORKSPACE
+    # chunk = 0 is held to the size of the chunk it resolves to: 32-token
+    # chunks for one sequence of 32768 tokens (168 MiB)
+    assert gdn.prefill_auto_chunk(1, 32768, 16, 32, 128, 128) == 32
+    assert call(**dict(big, n_tokens=32768, chunk=0)) == E.GDN_ERR_WORKSPACE
     assert gdn.prefill_workspace_size(1, 4096, 16, 32, 128, 128, 64) <= \
         gdn.PREFILL_SCRATCH_MAX_BYTES
     # the header and the binding agree on the array's size
