@@ -80,7 +80,7 @@ int32_t auto_chunk(int32_t n_seqs, int64_t n_tokens, int32_t hv, int32_t d) {
   if (avg <= r.c32) return 32;
   auto whole_chain = [&](int c) {
     return !gdn::uses_wave_carry(n_seqs, n_tokens, c) &&
-           !gdn::uses_tile_carry(n_seqs, n_tokens, hv, c);
+           !gdn::uses_tile_carry(n_seqs, n_tokens, hv, d, c);
   };
   return (whole_chain(32) && (d >= 64 || whole_chain(64))) ? 32 : 64;
 }
@@ -111,8 +111,9 @@ ChunkArg parse_chunk(int32_t chunk) {
 // The carry of a chunked call (chunk resolved): the per-tile carry when
 // forced, or when no segment length is forced and the whole-chain carry
 // would not fill the chip.
-bool tile_carry(const ChunkArg &c, int32_t n_seqs, int64_t n_tokens, int32_t hv, int32_t chunk) {
-  return c.tiles || (c.seg == 0 && gdn::uses_tile_carry(n_seqs, n_tokens, hv, chunk));
+bool tile_carry(const ChunkArg &c, int32_t n_seqs, int64_t n_tokens, int32_t hv, int32_t d,
+                int32_t chunk) {
+  return c.tiles || (c.seg == 0 && gdn::uses_tile_carry(n_seqs, n_tokens, hv, d, chunk));
 }
 
 // Workspace bytes for a resolved chunk size. The token-serial path uses none;
@@ -120,9 +121,9 @@ bool tile_carry(const ChunkArg &c, int32_t n_seqs, int64_t n_tokens, int32_t hv,
 size_t required_workspace(int32_t n_seqs, int64_t n_tokens, int32_t hqk, int32_t hv, int32_t d,
                           int32_t chunk, const ChunkArg &c) {
   if (chunk == 1) return 256;
-  const int L = gdn::chain_segment_chunks(n_tokens, hv, chunk, c.seg);
+  const int L = gdn::chain_segment_chunks(n_seqs, n_tokens, hv, chunk, c.seg);
   return gdn::prefill_workspace_layout(n_seqs, n_tokens, hqk, hv, d, chunk, L,
-                                       tile_carry(c, n_seqs, n_tokens, hv, chunk))
+                                       tile_carry(c, n_seqs, n_tokens, hv, d, chunk))
       .total;
 }
 
@@ -185,7 +186,7 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
   if (!cu_seqlens || !final_state) return GDN_ERR_INVALID_ARG;
   if (n_tokens > 0 && (!q || !k || !v || !o || !gate_present(g, beta, gate)))
     return GDN_ERR_INVALID_ARG;
-  const int seg_chunks = chunk == 1 ? 0 : gdn::chain_segment_chunks(n_tokens, hv, chunk, ca.seg);
+  const int seg_chunks = chunk == 1 ? 0 : gdn::chain_segment_chunks(n_seqs, n_tokens, hv, chunk, ca.seg);
   if (use_scratch) {
     // Size first (no HIP call for a refused size), then the device's array.
     if (required_workspace(n_seqs, n_tokens, hqk, hv, dk, chunk, ca) >
@@ -215,7 +216,7 @@ gdn_status prefill_impl(const void *q, const void *k, const void *v, const float
   // work-group carry's fixed cost then outweighs its per-chunk speed.
   a.wave_carry = gdn::uses_wave_carry(n_seqs, n_tokens, chunk);
   a.seg_chunks = seg_chunks;
-  a.tile_carry = tile_carry(ca, n_seqs, n_tokens, hv, chunk);
+  a.tile_carry = tile_carry(ca, n_seqs, n_tokens, hv, dk, chunk);
   a.dtype = dtype;
   a.workspace = workspace;
   a.stream = stream;

@@ -73,12 +73,17 @@ inline int64_t chunk_bound(int n_seqs, int64_t n_tokens, int chunk) {
   return (n_tokens + chunk - 1) / chunk + n_seqs;
 }
 // Chunks per segment of the whole-chain carry: `requested` if positive, else
-// enough that the segments of all chains give about kChainUnits work-groups.
+// for batches of fewer than kChainUnits chains as many segments per
+// average-length sequence as keep all (segment, value head) work-groups in
+// one round of kChainUnits, and for more chains the length at which the whole
+// batch as one chain would give kChainUnits work-groups (so that only chains
+// far longer than the average are cut).
 constexpr int kChainUnits = 256;
 // The whole-chain carry fills the chip when the batch has at least this many
 // (sequence, value head) chains, one work-group each, or when its automatic
 // segments are at least kChainMinSegment chunks long (long chains, cut into
-// enough segments, whose map and composition launches are then amortised).
+// enough segments, whose map and composition launches are then amortised),
+// and at d = 128 from 128 chains on with medium lengths (uses_tile_carry).
 // Otherwise the per-tile carry spreads every chain over D/16 work-groups.
 // Measured (d = 128, 16/32 heads, C = 64): 66K tokens in 16 sequences (512
 // chains) whole-chain 1.07-1.10 ms, per-tile 1.43 ms; 2 x 32768 tokens (64
@@ -88,7 +93,7 @@ constexpr int kChainUnits = 256;
 constexpr int64_t kChainCarryMinChains = 256;
 constexpr int kChainMinSegment = 64;
 constexpr int kMinSegmentChunks = 4;
-int chain_segment_chunks(int64_t n_tokens, int hv, int chunk, int requested);
+int chain_segment_chunks(int n_seqs, int64_t n_tokens, int hv, int chunk, int requested);
 // The whole-chain carry runs unless the average sequence fits in one chunk
 // (then the single-wave carry does).
 inline bool uses_wave_carry(int n_seqs, int64_t n_tokens, int chunk) {
@@ -97,7 +102,7 @@ inline bool uses_wave_carry(int n_seqs, int64_t n_tokens, int chunk) {
 // The per-tile carry unless the whole-chain carry fills the chip (see
 // kChainCarryMinChains): every chain is then spread over D/16 work-groups
 // without segments.
-bool uses_tile_carry(int n_seqs, int64_t n_tokens, int hv, int chunk);
+bool uses_tile_carry(int n_seqs, int64_t n_tokens, int hv, int d, int chunk);
 PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,
                                           int hv, int d, int chunk, int seg_chunks, bool tile);
 

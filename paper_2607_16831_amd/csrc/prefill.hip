@@ -696,16 +696,42 @@ __global__ __launch_bounds__(256) void chunk_wave_kernel(
 // ============================================================ host side
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-int chain_segment_chunks(int64_t n_tokens, int hv, int chunk, int requested) {
+int chain_segment_chunks(int n_seqs, int64_t n_tokens, int hv, int chunk, int requested) {
   if (requested > 0) return requested;
   const int64_t nck = (n_tokens + chunk - 1) / chunk;  // chunks of the longest possible chain
-  const int64_t l = (nck * hv + kChainUnits - 1) / kChainUnits;
+  const int64_t chains = (int64_t)std::max(n_seqs, 1) * hv;
+  int64_t l;
+  if (chains >= kChainUnits) {
+    // The chains fill the chip: only a chain far longer than the average is
+    // cut, into segments of the length at which the whole batch as one chain
+    // would give kChainUnits work-groups.
+    l = (nck * hv + kChainUnits - 1) / kChainUnits;
+  } else {
+    // Sequences of the average length are cut into as many segments as keep
+    // every (segment, value head) in one round of kChainUnits work-groups,
+    // and not at all when two would not fit: 6 x 4096 tokens (192 chains) at
+    // C = 32 ran 473 us in two segments per sequence, 360 us in one.
+    const int64_t avg = (nck + std::max(n_seqs, 1) - 1) / std::max(n_seqs, 1);
+    const int64_t g = kChainUnits / chains;
+    l = (avg + g - 1) / g;
+  }
   return (int)std::min<int64_t>(std::max<int64_t>(l, kMinSegmentChunks), 1 << 20);
 }
 
-bool uses_tile_carry(int n_seqs, int64_t n_tokens, int hv, int chunk) {
-  return (int64_t)n_seqs * hv < kChainCarryMinChains &&
-         chain_segment_chunks(n_tokens, hv, chunk, 0) < kChainMinSegment;
+bool uses_tile_carry(int n_seqs, int64_t n_tokens, int hv, int d, int chunk) {
+  const int64_t chains = (int64_t)n_seqs * hv;
+  if (chains >= kChainCarryMinChains ||
+      chain_segment_chunks(n_seqs, n_tokens, hv, chunk, 0) >= kChainMinSegment)
+    return false;
+  if (d < 128 || n_seqs <= 0) return true;
+  // d = 128: eight 16-row tiles per chain make the per-tile carry's
+  // work-groups many once chains reach the low hundreds. Measured (16/32
+  // heads, N equal sequences of L tokens, each carry with its best chunk):
+  // 7 x 1024 tokens whole-chain 97 against 140 us, 6 x 512 57 against 74,
+  // 5 x 256 37 against 45, 4 x 512 53 against 54; the per-tile carry stays
+  // ahead at 4 x 256 (36 against 40 us) and 5 x 128 (31 against 32).
+  const int64_t avg = (n_tokens + n_seqs - 1) / n_seqs;
+  return !(chains >= 192 || (chains >= 160 && avg >= 256) || (chains >= 128 && avg >= 512));
 }
 
 PrefillWorkspace prefill_workspace_layout(int n_seqs, int64_t n_tokens, int hqk,

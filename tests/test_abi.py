@@ -91,9 +91,10 @@ def test_auto_chunk_rule():
              ((4096, 4096), (512, 2048), (128, 128 * 12), (64, 64 * 40), (1, 4096),
               (1, 8192), (3, 12288), (16, 66000), (2, 65536), (4, 16384), (1, 16384))]
     # measured choices at d = 128: token-serial for single tokens, then 16, 32,
-    # 64 while 32 would take the per-tile carry (few, short chains), 32 where
-    # 32 takes the whole-chain carry (many chains, or long ones)
-    assert picks == [1, 16, 16, 32, 64, 64, 64, 32, 32, 32, 32]
+    # 64 while 32 would take the per-tile carry (few, short chains: one
+    # sequence of 4096 or 8192 tokens), 32 where 32 takes the whole-chain
+    # carry (many chains, or long ones: 3 x 4096 tokens and up)
+    assert picks == [1, 16, 16, 32, 64, 64, 32, 32, 32, 32, 32]
     # at d = 32 only where 64 takes the whole-chain carry too
     assert ac(4, 16384, 16, 32, 32, 32) == 64 and ac(4, 16384, 16, 32, 64, 64) == 32
     assert ac(16, 66000, 16, 32, 32, 32) == 32
