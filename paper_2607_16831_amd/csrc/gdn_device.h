@@ -56,6 +56,24 @@ struct Elem<__bf16> {
   }
 };
 
+// The bits of one input element, read ahead of its use and converted there.
+template <typename T>
+struct RawElem;
+template <>
+struct RawElem<__bf16> {
+  static __device__ __forceinline__ uint32_t load(const __bf16 *p) {
+    return *reinterpret_cast<const uint16_t *>(p);
+  }
+  static __device__ __forceinline__ float cvt(uint32_t b) { return bf16_bits_to_f32(b); }
+};
+template <>
+struct RawElem<float> {
+  static __device__ __forceinline__ uint32_t load(const float *p) {
+    return *reinterpret_cast<const uint32_t *>(p);
+  }
+  static __device__ __forceinline__ float cvt(uint32_t b) { return __uint_as_float(b); }
+};
+
 template <>
 struct Elem<float> {
   static __device__ __forceinline__ uint4 load8(const float *p) {

@@ -262,12 +262,18 @@ __device__ __forceinline__ void carry_compute_xu(
   uint4 fa[F::KS];   // T' rows of block ib (global)
   uint4 ka[F::DS];   // K rows of block ib (LDS)
   uint4 kt[F::KS];   // K^T operands of key tile `wave` (LDS)
-  float vv[4], ge[4], he[4], glast = 0.f;
+  // V is kept as the input's bits until phase 1 uses it: converting it where
+  // it is read (phase 3 of the chunk before) made each conversion wait for
+  // its LDS read there, on the chunk's critical path (4096 tokens: 76.6 ->
+  // 75.5 us per call). Reading the output wavefronts' decay factor a phase
+  // early instead was slower (77.4 us).
+  uint32_t vb[4];
+  float ge[4], he[4], glast = 0.f;
   auto fetch_lds = [&](int b) {  // V, decay factors, then K^T and K rows of buffer b
     if (blk) {
       const TIn *vt = reinterpret_cast<const TIn *>(L.Vl[b]);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) vv[e] = Elem<TIn>::load1(&vt[(tb + e) * 16 + l16]);
+      for (int e = 0; e < 4; ++e) vb[e] = RawElem<TIn>::load(&vt[(tb + e) * 16 + l16]);
       const float4 ge4 = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
       const float4 he4 = *reinterpret_cast<const float4 *>(&L.Dl[b][C + tb]);
       ge[0] = ge4.x; ge[1] = ge4.y; ge[2] = ge4.z; ge[3] = ge4.w;
@@ -302,8 +308,8 @@ __device__ __forceinline__ void carry_compute_xu(
 #pragma unroll
       for (int s = 0; s < F::DS; ++s) xs = mfma_16x16x32(ka[s], bs[s], xs);
       *reinterpret_cast<uint2 *>(&L.Yl[y_slot(ib, l16, g4)]) =
-          pack4_bf16(vv[0] - ge[0] * xs[0], vv[1] - ge[1] * xs[1], vv[2] - ge[2] * xs[2],
-                     vv[3] - ge[3] * xs[3]);
+          pack4_bf16(RawElem<TIn>::cvt(vb[0]) - ge[0] * xs[0], RawElem<TIn>::cvt(vb[1]) - ge[1] * xs[1],
+                     RawElem<TIn>::cvt(vb[2]) - ge[2] * xs[2], RawElem<TIn>::cvt(vb[3]) - ge[3] * xs[3]);
     }
     lds_barrier();
     // ---- phase 2: U = T' Y and exp(gamma_last - gamma) U
