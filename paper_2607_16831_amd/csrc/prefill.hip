@@ -328,15 +328,17 @@ __global__ __launch_bounds__(256, HPW == 1 ? 8 : 4) void chunk_local_kernel(
                  : make_uint4(0, 0, 0, 0);
   // gamma: inclusive prefix sum of g over the chunk, lane t holding token t
   // (lanes past the end and past C hold g = 0: they repeat the last value).
+  // Decay factors for the carry, exp(gamma_i) and exp(gamma_last - gamma_i),
+  // of head `wave`: stored after the barrier below, whose wait for the K and
+  // Q loads would otherwise also wait for these stores to complete.
+  float dec_a = 0.f, dec_b = 0.f;
 #pragma unroll
   for (int hh = 0; hh < HPW; ++hh) {
     const float gam = wave_prefix_sum(gl[hh]);
-    if (wave == hh && lane < C) {
-      // decay factors for the carry: exp(gamma_i) and exp(gamma_last - gamma_i)
+    if (wave == hh) {
       const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gam), C - 1));
-      const int64_t slot = slot0 + hh;
-      dec_ws[slot * 2 * C + lane] = __expf(gam);
-      dec_ws[slot * 2 * C + C + lane] = __expf(glast - gam);
+      dec_a = __expf(gam);
+      dec_b = __expf(glast - gam);
     }
     // per-wavefront copies of gamma and beta for the decay masks (outside
     // the K tile's space: Q K^T is masked before the tile is released)
@@ -345,6 +347,11 @@ __global__ __launch_bounds__(256, HPW == 1 ? 8 : 4) void chunk_local_kernel(
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+  if (wave < HPW && lane < C) {
+    const int64_t slot = slot0 + wave;
+    dec_ws[slot * 2 * C + lane] = dec_a;
+    dec_ws[slot * 2 * C + C + lane] = dec_b;
+  }
 
   // ---- for the per-tile carry (qfrag not null): Q of this chunk in the
   // A-operand order of Q S^T, block ib, step s, lane (l16, g4) holding
