@@ -33,10 +33,11 @@ namespace gdn {
 // X -> Y -> U -> state; each phase reads from LDS only what the phase before
 // produced (S^T, Y, U). Everything else a phase needs -- K rows and K^T
 // operands, V and the decay factors -- is read into registers a phase or
-// more ahead: waves 0-3 read those of chunk c + 1 right after the state
-// update of chunk c (the reads stay in flight across the barrier), waves
-// 4-7 their K^T operands in phase 1. Outputs go from registers straight to
-// global memory.
+// more ahead: waves 0-3 read the K rows, V and exp(gamma) of chunk c + 1
+// right after the state update of chunk c (the K-row reads stay in flight
+// across the barrier) and their K^T operands in phase 1, waves 4-7 their
+// K^T operands in phase 1 too. Outputs go from registers straight to global
+// memory.
 //
 // Global reads go through buffer resources: rows past the end of the
 // sequence read as zero (beta is zero there, so they add exact zeros) and
@@ -209,7 +210,8 @@ __device__ __forceinline__ void carry_loader(
 
 // ---------------------------------------------------------------- compute
 // Per chunk c, three phases separated by work-group barriers:
-//   1. waves 0-3: X = K S^T for their token block, Y = V - exp(gamma) X.
+//   1. waves 0-3: X = K S^T for their token block, Y = V - exp(gamma) X;
+//      then T' of chunk c + 1 and the K^T operands of chunk c.
 //      waves 4-7: O of chunk c-1 = exp(gamma) Q S^T + P U (their operands
 //      were kept from chunk c-1; U of chunk c-1 is still in LDS), stored to
 //      global memory; the K^T operands of chunk c.
@@ -270,20 +272,13 @@ __device__ __forceinline__ void carry_compute_xu(
   // early instead was slower (77.4 us).
   uint32_t vb[4];
   float ge[4], he[4], glast = 0.f;
-  auto fetch_lds = [&](int b) {  // V, decay factors, then K^T and K rows of buffer b
+  auto fetch_lds = [&](int b) {  // V, exp(gamma), then K rows of buffer b
     if (blk) {
       const TIn *vt = reinterpret_cast<const TIn *>(L.Vl[b]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) vb[e] = RawElem<TIn>::load(&vt[(tb + e) * 16 + l16]);
       const float4 ge4 = *reinterpret_cast<const float4 *>(&L.Dl[b][tb]);
-      const float4 he4 = *reinterpret_cast<const float4 *>(&L.Dl[b][C + tb]);
       ge[0] = ge4.x; ge[1] = ge4.y; ge[2] = ge4.z; ge[3] = ge4.w;
-      he[0] = he4.x; he[1] = he4.y; he[2] = he4.z; he[3] = he4.w;
-    }
-    glast = L.Dl[b][C - 1];
-    if (own) {
-#pragma unroll
-      for (int s = 0; s < F::KS; ++s) kt[s] = kt_operand<D>(L.Kn[b], wave, s, l16, g4);
     }
     if (blk) {
 #pragma unroll
@@ -322,7 +317,26 @@ __device__ __forceinline__ void carry_compute_xu(
       __builtin_amdgcn_sched_barrier(0);
       load_t(fnext, lc + 1);
     }
-    lds_barrier();
+    // Operands used later in this chunk: exp(gamma_last - gamma) for phase 2,
+    // gamma_last and the K^T operands for phase 3. Read here, in the wait for
+    // the output wavefronts, rather than with the next chunk's operands at
+    // the end of phase 3, whose barrier they delayed (carry kernel at 4096
+    // tokens 55.2 -> 54.4 us; outputs bitwise unchanged). Moving the rest of
+    // that read (V, exp(gamma), K rows) into phase 2 gained nothing more.
+    {
+      const int b = lc % CC::NB;
+      if (blk) {
+        const float4 he4 = *reinterpret_cast<const float4 *>(&L.Dl[b][C + tb]);
+        he[0] = he4.x; he[1] = he4.y; he[2] = he4.z; he[3] = he4.w;
+      }
+      glast = L.Dl[b][C - 1];
+      if (own) {
+#pragma unroll
+        for (int s = 0; s < F::KS; ++s) kt[s] = kt_operand<D>(L.Kn[b], wave, s, l16, g4);
+      }
+    }
+    // the Y stores are complete; the K^T reads may stay in flight
+    lds_barrier_keep<((F::NKT == 8) ? 2 * F::KS : 0)>();
     // ---- phase 2: U = T' Y and exp(gamma_last - gamma) U
     if (blk) {
       uint4 by[F::KS];
@@ -339,14 +353,14 @@ __device__ __forceinline__ void carry_compute_xu(
     }
     lds_barrier();
     // ---- phase 3: state update, then chunk lc + 1's LDS operands, whose
-    // K^T and K reads may stay in flight across the barrier
+    // K-row reads may stay in flight across the barrier
     if (own) {
       state_update<D, C, TIn>(L, S, kt, glast, wave, l16, g4);
       asm volatile("" ::"v"(S) : "memory");
     }
     if (lc + 1 < nch) {
       fetch_lds((lc + 1) % CC::NB);
-      lds_barrier_keep<((F::NKT == 8) ? 2 * F::KS : 0) + ((F::NIB == 4) ? F::DS : 0)>();
+      lds_barrier_keep<((F::NIB == 4) ? F::DS : 0)>();
     } else {
       lds_barrier();
     }
