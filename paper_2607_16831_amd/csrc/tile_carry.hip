@@ -150,12 +150,28 @@ constexpr int loader_copies() {
   for (int i = 0; i < CC::SLOTS; ++i) n += (CC::NLW * i + LW < CC::M) ? 1 : 0;
   return n;
 }
+// A loader issues a chunk's copies in three parts, one per phase: slots
+// [part_lo(p), part_lo(p + 1)) in part p.
+template <int D, int C, typename TIn>
+constexpr int part_lo(int p) { return (CarryCfg<D, C, TIn>::SLOTS * p) / 3; }
+template <int D, int C, typename TIn, int LW>
+constexpr int part_copies(int p) {
+  using CC = CarryCfg<D, C, TIn>;
+  int n = 0;
+  for (int i = part_lo<D, C, TIn>(p); i < part_lo<D, C, TIn>(p + 1); ++i)
+    n += (CC::NLW * i + LW < CC::M) ? 1 : 0;
+  return n;
+}
 
 // Loader wavefront LW (a template parameter, so that the kind of each of its
-// copies is known when compiling). The copies of chunk lc + NA are issued at
-// the start of chunk lc into the buffer chunk lc - 1 used, and chunk lc + 1
-// must have landed before the second barrier of chunk lc: waves 0-3 read it
-// in phase 3.
+// copies is known when compiling). The copies of chunk lc + NA go into the
+// buffer chunk lc - 1 used, a third of them before each barrier of chunk lc,
+// and chunk lc + 1 must have landed before the second barrier of chunk lc:
+// waves 0-3 read it in phase 3. Issuing a buffer-to-LDS copy takes a
+// wavefront tens of cycles while the compute wavefronts load and store too;
+// issued all at the start of the chunk, the copies held the first barrier
+// past the compute wavefronts' phase 1 (carry kernel at 4096 tokens 54.0 ->
+// 52.5 us; two parts, before the second and third barriers: 53.5 us).
 template <int D, int C, typename TIn, int LW>
 __device__ __forceinline__ void carry_loader(
     CarryLds<D, C, TIn> &L, int lane, const uint16_t *__restrict__ ksrc, int kstride,
@@ -193,17 +209,28 @@ __device__ __forceinline__ void carry_loader(
     wait_vm<0>();
   lds_barrier();
 
+  auto issue_part = [&](int lc, auto part) {  // part p of chunk lc's copies
+    constexpr int p = decltype(part)::value;
+    const CopyRes R = res(lc);
+#pragma unroll
+    for (int i = part_lo<D, C, TIn>(p); i < part_lo<D, C, TIn>(p + 1); ++i)
+      issue_copy<D, C, TIn>(L, lc % CC::NB, R, CC::NLW * i + LW, off[i]);
+  };
   for (int lc = 0; lc < nch; ++lc) {
-    if (lc + NA < nch) issue(lc + NA);
+    const bool more = lc + NA < nch;
+    if (more) issue_part(lc + NA, std::integral_constant<int, 0>{});
     lds_barrier();
+    if (more) issue_part(lc + NA, std::integral_constant<int, 1>{});
     // Chunk lc + 1 must have landed. While copies are still issued every
-    // chunk, those of the NA - 1 later chunks may stay in flight; near the
-    // end everything is waited for.
-    if (lc + NA < nch)
-      wait_vm<(NA - 1) * NCP>();
+    // chunk, those of chunk lc + 2 and the parts of chunk lc + NA issued so
+    // far may stay in flight; near the end everything is waited for.
+    static_assert(NA == 3, "chunks in flight");
+    if (more)
+      wait_vm<NCP + part_copies<D, C, TIn, LW>(0) + part_copies<D, C, TIn, LW>(1)>();
     else
       wait_vm<0>();
     lds_barrier();
+    if (more) issue_part(lc + NA, std::integral_constant<int, 2>{});
     lds_barrier();
   }
 }
