@@ -34,9 +34,9 @@ namespace gdn {
 // produced (S^T, Y, U). Everything else a phase needs -- K rows and K^T
 // operands, V and the decay factors -- is read into registers a phase or
 // more ahead: waves 0-3 read the K rows, V and exp(gamma) of chunk c + 1
-// right after the state update of chunk c (the K-row reads stay in flight
-// across the barrier) and their K^T operands in phase 1, waves 4-7 their
-// K^T operands in phase 1 too. Outputs go from registers straight to global
+// in phase 2 of chunk c (the K-row reads stay in flight across the barrier)
+// and their K^T operands in phase 1, waves 4-7 their K^T operands in
+// phase 1 too. Outputs go from registers straight to global
 // memory.
 //
 // Global reads go through buffer resources: rows past the end of the
@@ -166,8 +166,8 @@ constexpr int part_copies(int p) {
 // Loader wavefront LW (a template parameter, so that the kind of each of its
 // copies is known when compiling). The copies of chunk lc + NA go into the
 // buffer chunk lc - 1 used, a third of them before each barrier of chunk lc,
-// and chunk lc + 1 must have landed before the second barrier of chunk lc:
-// waves 0-3 read it in phase 3. Issuing a buffer-to-LDS copy takes a
+// and chunk lc + 1 must have landed before the first barrier of chunk lc:
+// waves 0-3 read it in phase 2. Issuing a buffer-to-LDS copy takes a
 // wavefront tens of cycles while the compute wavefronts load and store too;
 // issued all at the start of the chunk, the copies held the first barrier
 // past the compute wavefronts' phase 1 (carry kernel at 4096 tokens 54.0 ->
@@ -219,16 +219,16 @@ __device__ __forceinline__ void carry_loader(
   for (int lc = 0; lc < nch; ++lc) {
     const bool more = lc + NA < nch;
     if (more) issue_part(lc + NA, std::integral_constant<int, 0>{});
-    lds_barrier();
-    if (more) issue_part(lc + NA, std::integral_constant<int, 1>{});
     // Chunk lc + 1 must have landed. While copies are still issued every
-    // chunk, those of chunk lc + 2 and the parts of chunk lc + NA issued so
-    // far may stay in flight; near the end everything is waited for.
+    // chunk, those of chunk lc + 2 and the part of chunk lc + NA just issued
+    // may stay in flight; near the end everything is waited for.
     static_assert(NA == 3, "chunks in flight");
     if (more)
-      wait_vm<NCP + part_copies<D, C, TIn, LW>(0) + part_copies<D, C, TIn, LW>(1)>();
+      wait_vm<NCP + part_copies<D, C, TIn, LW>(0)>();
     else
       wait_vm<0>();
+    lds_barrier();
+    if (more) issue_part(lc + NA, std::integral_constant<int, 1>{});
     lds_barrier();
     if (more) issue_part(lc + NA, std::integral_constant<int, 2>{});
     lds_barrier();
@@ -242,10 +242,11 @@ __device__ __forceinline__ void carry_loader(
 //      waves 4-7: O of chunk c-1 = exp(gamma) Q S^T + P U (their operands
 //      were kept from chunk c-1; U of chunk c-1 is still in LDS), stored to
 //      global memory; the K^T operands of chunk c.
-//   2. waves 0-3: U = T' Y and exp(gamma_last - gamma) U.
+//   2. waves 0-3: U = T' Y and exp(gamma_last - gamma) U; then chunk
+//      c + 1's K rows, V and exp(gamma).
 //      waves 4-7: Q S^T (S is still the state entering chunk c).
 //   3. all eight: S^T <- exp(gamma_last) S^T + K^T (exp(gamma_last - gamma) U)
-//      for their key tile; waves 0-3 then read chunk c + 1's operands.
+//      for their key tile.
 // The chain from one state to the next runs through phases 1-3 on waves 0-3
 // and the update; the output work fills the phases where it would idle.
 template <int D, int C, typename TIn>
@@ -293,10 +294,10 @@ __device__ __forceinline__ void carry_compute_xu(
   uint4 ka[F::DS];   // K rows of block ib (LDS)
   uint4 kt[F::KS];   // K^T operands of key tile `wave` (LDS)
   // V is kept as the input's bits until phase 1 uses it: converting it where
-  // it is read (phase 3 of the chunk before) made each conversion wait for
-  // its LDS read there, on the chunk's critical path (4096 tokens: 76.6 ->
-  // 75.5 us per call). Reading the output wavefronts' decay factor a phase
-  // early instead was slower (77.4 us).
+  // it is read (then phase 3 of the chunk before, now phase 2) made each
+  // conversion wait for its LDS read there, on the chunk's critical path
+  // (4096 tokens: 76.6 -> 75.5 us per call). Reading the output wavefronts'
+  // decay factor a phase early instead was slower (77.4 us).
   uint32_t vb[4];
   float ge[4], he[4], glast = 0.f;
   auto fetch_lds = [&](int b) {  // V, exp(gamma), then K rows of buffer b
@@ -348,8 +349,9 @@ __device__ __forceinline__ void carry_compute_xu(
     // gamma_last and the K^T operands for phase 3. Read here, in the wait for
     // the output wavefronts, rather than with the next chunk's operands at
     // the end of phase 3, whose barrier they delayed (carry kernel at 4096
-    // tokens 55.2 -> 54.4 us; outputs bitwise unchanged). Moving the rest of
-    // that read (V, exp(gamma), K rows) into phase 2 gained nothing more.
+    // tokens 55.2 -> 54.4 us; outputs bitwise unchanged). The next chunk's
+    // operands themselves are read in phase 2 (52.1 -> 51.3 us once the
+    // loaders issued their copies over the three phases).
     {
       const int b = lc % CC::NB;
       if (blk) {
@@ -378,19 +380,21 @@ __device__ __forceinline__ void carry_compute_xu(
       *reinterpret_cast<uint2 *>(&L.Uh[y_slot(ib, l16, g4)]) =
           pack4_bf16(he[0] * u[0], he[1] * u[1], he[2] * u[2], he[3] * u[3]);
     }
-    lds_barrier();
-    // ---- phase 3: state update, then chunk lc + 1's LDS operands, whose
-    // K-row reads may stay in flight across the barrier
-    if (own) {
-      state_update<D, C, TIn>(L, S, kt, glast, wave, l16, g4);
-      asm volatile("" ::"v"(S) : "memory");
-    }
+    // chunk lc + 1's LDS operands, whose K-row reads may stay in flight
+    // across the barrier; its copies landed before the first barrier
     if (lc + 1 < nch) {
+      __builtin_amdgcn_sched_barrier(0);
       fetch_lds((lc + 1) % CC::NB);
       lds_barrier_keep<((F::NIB == 4) ? F::DS : 0)>();
     } else {
       lds_barrier();
     }
+    // ---- phase 3: state update
+    if (own) {
+      state_update<D, C, TIn>(L, S, kt, glast, wave, l16, g4);
+      asm volatile("" ::"v"(S) : "memory");
+    }
+    lds_barrier();
   };
   for (int lc = 0; lc < nch; lc += 2) {
     step(lc, fa, fb);
