@@ -220,6 +220,20 @@ def test_prefill_shapes(d, chunk, dtype):
                o_bar=ob, s_bar=sb)
 
 
+@pytest.mark.parametrize("chunk", [16, 32, 64])
+def test_tile_carry_chunk_counts(chunk):
+    """The per-tile carry on one sequence of each length from 1 to 9 chunks
+    of 64 tokens, each with a ragged tail: the loaders' look-ahead of three
+    chunks, issued in parts over the phases, starts, runs and drains at
+    every count."""
+    dev = require_gpu()
+    lengths = tuple(64 * n - 5 for n in range(1, 10))
+    w = synth.PREFILL_4K.replace(seq_len=None, lengths=lengths, n_seqs=len(lengths), hqk=1,
+                                 hv=2, g_mu=-3.0, state_std=0.1, seed=43)
+    check_full("tile_counts_C%d" % chunk, synth.make(w), dev,
+               chunk=chunk | gdn.CHUNK_TILE_CARRY)
+
+
 def test_prefill_alias_in_place():
     dev = require_gpu()
     w = synth.PREFILL_4K.replace(seq_len=None, lengths=(90, 7), n_seqs=2,
